@@ -1,0 +1,269 @@
+"""Benchmark of the Sketch&Walk prefill hot path on one MI355X.
+
+One step = every layer of the Llama-3-8B-shaped workload (32 layers, 32 query
+/ 8 KV heads, head dim 128, 32768 tokens, block 128, bf16, density 20%) run
+through the full path: sketch scores, walk update, top-tau selection and
+block-sparse attention, with inputs already resident in HBM.
+
+Prints one JSON line. ``value`` is the sparse-prefill throughput in TFLOP/s on
+the attention FLOPs the selection makes the kernel execute (unmasked query/key
+pairs, 4*d flop each), divided by the wall time of the whole step (sketch,
+walk and selection included). ``roofline`` describes the attention kernel
+alone: its algorithmic FLOPs per launch over its average launch time measured
+with HIP events on the launch stream, against the bf16 dense MFMA peak.
+``cpu_baseline`` is the fp64 oracle timed on a bounded sample of the same
+layer on this host's cores.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0
+
+
+def attention_flops(idx: np.ndarray, cnt: np.ndarray, cu, B: int, h_q: int, d: int):
+    """(unmasked, tile) FLOPs of one layer's sparse attention: 4*d per
+    (query, key) pair the selection admits; tile FLOPs count the diagonal
+    block in full."""
+    alg = 0
+    tile = 0
+    r = 0
+    for a, e in zip(cu[:-1], cu[1:]):
+        n = int(e) - int(a)
+        b = -(-n // B)
+        for i in range(b):
+            ci = min(B, n - i * B)
+            for j in idx[r, :cnt[r]]:
+                cj = min(B, n - int(j) * B)
+                alg += ci * (ci + 1) // 2 if j == i else ci * cj
+                tile += ci * cj
+            r += 1
+    return 4 * d * h_q * alg, 4 * d * h_q * tile
+
+
+def cpu_baseline(Qh, Kh, Vh, cu, B, signs, cols, s, pct, pairs, seed=0):
+    """Times the fp64 oracle on one layer: the full selection path (sketch,
+    walk, select) plus masked attention on `pairs` random (head, query block)
+    pairs; the attention time is scaled to the whole layer."""
+    import oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+    except Exception:  # pragma: no cover
+        cores = os.cpu_count() or 1
+    t0 = time.perf_counter()
+    Q = O.f64(Qh)
+    K = O.f64(Kh)
+    V = O.f64(Vh)
+    t_conv = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    sk = O.sketch_scores(Q, K, B, signs, cols)
+    R = O.walk_step(None, O.walk_weights(sk["A"], sk["c"], s))
+    sel, _ = O.select_blocks(R, pct=pct)
+    t_sel = time.perf_counter() - t0
+    h_q = Q.shape[0]
+    b = len(sel)
+    rng = np.random.default_rng(seed)
+    samp = [(int(rng.integers(h_q)), int(rng.integers(b))) for _ in range(pairs)]
+    t0 = time.perf_counter()
+    flops_s = 0
+    n = Q.shape[1]
+    d = Q.shape[2]
+    for (u, i) in samp:
+        O.sparse_attention_block(Q, K, V, B, sel[i], u, i)
+        ci = min(B, n - i * B)
+        for j in sel[i]:
+            cj = min(B, n - j * B)
+            flops_s += 4 * d * (ci * (ci + 1) // 2 if j == i else ci * cj)
+    t_attn = time.perf_counter() - t0
+    total_pairs = h_q * b
+    flops_layer = 0
+    for i in range(b):
+        ci = min(B, n - i * B)
+        for j in sel[i]:
+            cj = min(B, n - j * B)
+            flops_layer += 4 * d * h_q * (ci * (ci + 1) // 2 if j == i else ci * cj)
+    t_layer = t_sel + t_attn * (flops_layer / max(flops_s, 1))
+    return {
+        "value": flops_layer / t_layer / 1e12,
+        "unit": "TFLOP/s",
+        "cores": int(cores),
+        "kind": "oracle",
+        "sample": (f"layer 0 of the workload: full fp64 selection path ({t_sel:.1f} s) + masked "
+                   f"attention on {pairs} random (head, query-block) pairs of {total_pairs} "
+                   f"({t_attn:.1f} s), attention time scaled by executed FLOPs to the layer; "
+                   f"input conversion ({t_conv:.1f} s) excluded"),
+        "layer_seconds_extrapolated": t_layer,
+    }
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--layers", type=int, default=None, help="override layer count (debug only)")
+    ap.add_argument("--cpu-pairs", type=int, default=192)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU; --gpus must be 1"}))
+        print("bench.py: only --gpus 1 is supported (one GPU per run)", file=sys.stderr)
+        return 2
+
+    import torch
+    import synth
+    from paper_2602_07397_amd import binding as sw
+
+    dev = torch.device("cuda:0")
+    w = synth.WORKLOADS["llama8b"]
+    L = args.layers or w.layers
+    cu = synth.cu_seqlens(w.seqlens)
+    B = w.B
+    signs, cols = synth.srht_params(w.d, w.r, w.seed)
+    ts = torch.from_numpy(signs).to(dev)
+    tc = torch.from_numpy(cols).to(dev)
+
+    t0 = time.perf_counter()
+    layers = [synth.prefill_layer_inputs(w, l, device=dev) for l in range(L)]
+    torch.cuda.synchronize(dev)
+    print(f"[bench] generated {L} layers in {time.perf_counter() - t0:.1f} s", file=sys.stderr,
+          flush=True)
+
+    nb, nm, _ = sw.layout(cu, B)
+    kmax = sw.select_max_count(cu, B, density_pct=w.pct)
+    f64 = dict(dtype=torch.float64, device=dev)
+    bufs = {
+        "Qs": torch.empty((nb, w.r), **f64), "Ks": torch.empty((nb, w.r), **f64),
+        "A": torch.empty((nm,), **f64), "A_scale": torch.empty((1,), **f64),
+    }
+    ws = torch.empty((sw.sketch_workspace_bytes(w.h_q, w.h_kv, w.d, cu, B),), dtype=torch.uint8,
+                     device=dev)
+    Rbuf = [torch.empty((nm,), **f64), torch.empty((nm,), **f64)]
+    idx = [torch.empty((nb, kmax), dtype=torch.int32, device=dev) for _ in range(L)]
+    cnt = [torch.empty((nb,), dtype=torch.int32, device=dev) for _ in range(L)]
+    Obuf = torch.empty_like(layers[0][0])
+    stream = torch.cuda.current_stream(dev)
+
+    def step(events=None):
+        R = None
+        for l in range(L):
+            Q, K, V = layers[l]
+            if events is not None:
+                events[l][0].record(stream)
+            sk = sw.sketch_scores(Q, K, cu, B, ts, tc, out=bufs, workspace=ws)
+            if events is not None:
+                events[l][1].record(stream)
+            Rn = sw.walk_update(sk["A"], sk["A_scale"], w.s, cu, B, R, R_out=Rbuf[l & 1])
+            R = Rn
+            if events is not None:
+                events[l][2].record(stream)
+            sw.select_topk_blocks(R, cu, B, density_pct=w.pct, kmax=kmax, idx=idx[l], cnt=cnt[l])
+            if events is not None:
+                events[l][3].record(stream)
+            sw.sparse_attn_prefill(Q, K, V, cu, B, idx[l], cnt[l], kmax, O=Obuf)
+            if events is not None:
+                events[l][4].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize(dev)
+    print("[bench] warmup done", file=sys.stderr, flush=True)
+
+    flops_alg = 0
+    flops_tile = 0
+    per_layer_alg = []
+    for l in range(L):
+        a, t = attention_flops(idx[l].cpu().numpy(), cnt[l].cpu().numpy(), cu, B, w.h_q, w.d)
+        flops_alg += a
+        flops_tile += t
+        per_layer_alg.append(a)
+
+    # whole-step wall time
+    torch.cuda.synchronize(dev)
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    ev0.record(stream)
+    for _ in range(args.steps):
+        step()
+    ev1.record(stream)
+    torch.cuda.synchronize(dev)
+    ms_per_step = ev0.elapsed_time(ev1) / args.steps
+    print(f"[bench] timed {args.steps} steps: {ms_per_step:.2f} ms/step", file=sys.stderr, flush=True)
+
+    # per-phase breakdown (separate pass with events between the calls)
+    phase = np.zeros(4)
+    attn_times = []
+    for _ in range(max(1, min(args.steps, 3))):
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(L)]
+        step(evs)
+        torch.cuda.synchronize(dev)
+        for l in range(L):
+            for p in range(4):
+                phase[p] += evs[l][p].elapsed_time(evs[l][p + 1])
+            attn_times.append(evs[l][3].elapsed_time(evs[l][4]))
+    phase_frac = phase / phase.sum()
+    attn_ms = float(np.mean(attn_times))
+    achieved = (flops_alg / L) / (attn_ms * 1e-3) / 1e12
+
+    value = flops_alg / (ms_per_step * 1e-3) / 1e12
+    out = {
+        "metric": "sparse prefill TFLOP/s + decode tok/s at 20% density; sketch+select overhead %",
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1) with planted sink, local window and needles)",
+        "config": {
+            "workload": "llama8b-shaped sparse prefill: 32 layers, 32 q / 8 kv heads, head_dim 128, "
+                        "seq 32768, block 128, density 20%",
+            "layers": L, "h_q": w.h_q, "h_kv": w.h_kv, "head_dim": w.d, "seq_len": w.seqlens[0],
+            "block": B, "density_pct": w.pct, "sketch_dim": w.r, "sparsity_exponent": w.s,
+            "parallelism": "single GPU",
+        },
+        "executed_tflop_per_step": flops_alg / 1e12,
+        "tile_tflop_per_step": flops_tile / 1e12,
+        "overhead_pct": round(100.0 * float(phase_frac[:3].sum()), 3),
+        "phase_ms_per_step": {k: round(float(v) / max(1, min(args.steps, 3)), 4)
+                              for k, v in zip(("sketch", "walk", "select", "attention"), phase)},
+        "roofline": {
+            "kernel": "attn_prefill_bf16_kernel<128>",
+            "bound": "mfma",
+            "achieved": round(achieved, 2),
+            "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+            "traffic": None,
+            "avg_launch_ms": round(attn_ms, 4),
+            "flop_per_launch": flops_alg / L,
+        },
+    }
+    if not args.no_cpu_baseline:
+        Q, K, V = layers[0]
+        Qh, Kh, Vh = Q.cpu(), K.cpu(), V.cpu()
+        print("[bench] timing the oracle on the host", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(Qh, Kh, Vh, cu, B, signs, cols, w.s, w.pct,
+                                           args.cpu_pairs)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,178 @@
+/*
+ * sketchwalk.h - C ABI of the MI355X (gfx950) Sketch&Walk attention library.
+ *
+ * Method: Le et al., "Scout Before You Attend: Sketch-and-Walk Sparse
+ * Attention for Efficient LLM Inference". Each entry point below names the
+ * passage of the paper that defines what it computes.
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * - Pointers are DEVICE pointers unless marked [host]. The caller owns every
+ *   buffer; the library keeps no state between calls apart from a
+ *   thread-local error string.
+ * - `stream` is a hipStream_t passed as void* (NULL = the default stream).
+ *   Work is enqueued asynchronously; results are ready when the stream is.
+ * - Return value: SW_OK, or an error code with a message in
+ *   sw_last_error(). Arguments are validated on the host before anything is
+ *   enqueued; an invalid call enqueues nothing. SW_ERR_HIP reports a failed
+ *   launch. Faults inside a kernel surface at the caller's next
+ *   synchronisation.
+ * - Tensor pointers must be 16-byte aligned and sizes in elements are given
+ *   per argument. Element types: SW_F32 = float, SW_BF16 = bfloat16 stored as
+ *   uint16.
+ * - Sequences (prefill): `n_seqs` sequences are concatenated along the token
+ *   axis; cu_seqlens [host, n_seqs+1] holds cumulative lengths (cu[0] = 0,
+ *   every length >= 1, total N = cu[n_seqs]). Sequence s has
+ *   b_s = ceil(n_s / B) blocks. Block rows are numbered globally: sequence s
+ *   owns rows [bo_s, bo_s + b_s) with bo_s = sum_{t<s} b_t (nb = total).
+ *   Per-sequence b_s x b_s matrices are stored row-major back to back,
+ *   sequence s at element offset mo_s = sum_{t<s} b_t^2 (nm = total).
+ * - Q is [h_q][N][d], K and V are [h_kv][N][d] (head-major, row-major,
+ *   contiguous); h_q is a multiple of h_kv and query head u reads KV head
+ *   u / (h_q / h_kv).
+ * - Every output is deterministic: the same inputs give the same bits.
+ */
+#ifndef SKETCHWALK_H
+#define SKETCHWALK_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SW_ABI_VERSION 1
+
+#define SW_OK 0
+#define SW_ERR_INVALID_ARG 1
+#define SW_ERR_UNSUPPORTED 2
+#define SW_ERR_HIP 3
+
+#define SW_F32 0
+#define SW_BF16 1
+
+/* Forced-block flags for selection (paper Sec. 4.1 keeps the first and the
+   last key block of every query block). */
+#define SW_FORCE_FIRST 1u
+#define SW_FORCE_LAST 2u
+
+#define SW_MAX_SEQS 64          /* sequences per prefill call */
+#define SW_MAX_BLOCKS 4096      /* blocks per sequence */
+
+/* Message of the last failed call on this thread ("" if none). */
+const char* sw_last_error(void);
+
+/* SW_ABI_VERSION of the built library. */
+int sw_abi_version(void);
+
+/* Host-only layout query: nb (total block rows), nm (total matrix
+   elements, sum of b_s^2) and the largest b_s. No GPU work. */
+int sw_layout(int n_seqs, const int32_t* cu_seqlens /* [host] */, int B,
+              int64_t* nb, int64_t* nm, int32_t* max_b);
+
+/* Host-only: bytes of workspace sw_sketch_scores needs (>= 0), or -1 on
+   invalid arguments. */
+int64_t sw_sketch_workspace_bytes(int h_q, int h_kv, int d, int n_seqs,
+                                  const int32_t* cu_seqlens /* [host] */, int B);
+
+/* Host-only: the largest per-row budget tau_i a selection with these
+   parameters produces (the minimum valid `kmax`). Budget rule: k > 0 gives
+   tau_i = k, otherwise tau_i = ceil((i+1) * density_pct / 100) in integer
+   arithmetic; then tau_i is clamped to [|F_i|, i+1], F_i the forced set. */
+int sw_select_max_count(int n_seqs, const int32_t* cu_seqlens /* [host] */, int B,
+                        int k, int density_pct, uint32_t flags, int32_t* kmax);
+
+/*
+ * sw_sketch_scores - Small-World Sketching of one layer: paper Alg. 1
+ * steps 1-5 (Sec. 2.2; SRHT construction in the appendix lemma on the
+ * Hadamard transform guarantee).
+ *
+ *   qbar_i = mean over the tokens of block i of the head-averaged queries
+ *            (a partial last block averages the tokens it has); kbar likewise
+ *            over the KV heads.
+ *   Qs_i   = (1/sqrt(r)) * ((qbar_i * signs) H)[cols]   (H = +-1 Sylvester
+ *            Walsh-Hadamard matrix, natural order); Ks likewise.
+ *   A      = Qs Ks^T / sqrt(r) per sequence, with the entries whose key block
+ *            follows the query block set to 0 (causal).
+ *   A_scale[s] = max |A| over sequence s (0 when every score is 0; consumers
+ *            then use 1).
+ *
+ * dtype: SW_F32 or SW_BF16 (Q, K). d: power of two in [16, 256]. B: block
+ * size, multiple of 16, <= 1024. signs [d] int8 (+1/-1); cols [r] int32,
+ * distinct, in [0, d) (device data: values are reduced modulo d, never
+ * range-checked); 1 <= r <= d.
+ * Outputs (float64): Qs, Ks [nb][r]; A [nm]; A_scale [n_seqs]; Qbar, Kbar
+ * [nb][d] block means (optional, may be NULL).
+ * workspace: >= sw_sketch_workspace_bytes(...) bytes, 256-byte aligned.
+ */
+int sw_sketch_scores(int dtype, const void* Q, const void* K, int h_q, int h_kv, int d,
+                     int n_seqs, const int32_t* cu_seqlens /* [host] */, int B,
+                     const int8_t* signs, const int32_t* cols, int r,
+                     double* Qs, double* Ks, double* A, double* A_scale,
+                     double* Qbar, double* Kbar,
+                     void* workspace, int64_t workspace_bytes, void* stream);
+
+/*
+ * sw_walk_update - Sketch-Determined Walk: paper Sec. 2.3, Alg. 1 step 6,
+ * appendix lemma on walk accumulation across layers.
+ *
+ *   W = (A / c)^s element-wise (c = A_scale[s], or 1 where it is 0);
+ *   R_out = W if R_prev is NULL (first walked layer), else R_prev W;
+ *   then every row of R_out is divided by its largest magnitude (rows of
+ *   zeros stay zero). Both rescalings multiply rows by positive factors and
+ *   leave every ranking unchanged.
+ *
+ * A [nm] float64 from sw_sketch_scores (lower triangular per sequence);
+ * s: integer >= 1. R_prev, R_out [nm] float64; R_out must not alias R_prev
+ * or A. Sequences are independent.
+ */
+int sw_walk_update(const double* A, const double* A_scale, int s,
+                   int n_seqs, const int32_t* cu_seqlens /* [host] */, int B,
+                   const double* R_prev, double* R_out, void* stream);
+
+/*
+ * sw_select_topk_blocks - top-tau key blocks per query block: paper Alg. 1
+ * step 7, first/last blocks kept as in Sec. 4.1.
+ *
+ * Row i of sequence s ranks key blocks 0..i (causal). F_i = {0 if
+ * SW_FORCE_FIRST} U {i if SW_FORCE_LAST}; tau_i as in sw_select_max_count.
+ * The row keeps F_i plus the tau_i - |F_i| best other blocks by (R value
+ * descending, block index ascending).
+ *
+ * R [nm] float64. Outputs: idx [nb][kmax] int32 block indices ascending
+ * (entries past cnt[row] are -1); cnt [nb] int32 = tau_i. kmax must be at
+ * least sw_select_max_count(...). density_pct in [1, 100] (used when k <= 0).
+ */
+int sw_select_topk_blocks(const double* R, int n_seqs, const int32_t* cu_seqlens /* [host] */,
+                          int B, int k, int density_pct, uint32_t flags,
+                          int32_t* idx, int32_t* cnt, int kmax, void* stream);
+
+/*
+ * sw_sparse_attn_prefill - block-sparse causal attention on the original
+ * per-head Q, K, V over the selected blocks: paper Alg. 1 step 8.
+ *
+ * For query head u at token p of block i (sequence s), with g = u / G:
+ *   O[u][p] = sum_t softmax_t(scale * Q[u][p] . K[g][t]) V[g][t]
+ * over the tokens t <= p of the blocks idx[row][0..cnt[row]) (softmax
+ * renormalised over those keys only). scale <= 0 selects 1/sqrt(d).
+ *
+ * dtype SW_BF16 or SW_F32; d in {64, 128}; B in {64, 128} (other values
+ * return SW_ERR_UNSUPPORTED). O [h_q][N][d] in the input dtype. lse [h_q][N] float32
+ * natural-log sum-exp of the scaled logits (optional, may be NULL).
+ * idx/cnt as written by sw_select_topk_blocks (block indices ascending,
+ * each <= its row's block index; entries outside [0, i] are skipped and
+ * cnt is clamped to kmax, so malformed selections cannot read out of
+ * bounds).
+ */
+int sw_sparse_attn_prefill(int dtype, const void* Q, const void* K, const void* V,
+                           int h_q, int h_kv, int d,
+                           int n_seqs, const int32_t* cu_seqlens /* [host] */, int B,
+                           const int32_t* idx, const int32_t* cnt, int kmax, float scale,
+                           void* O, float* lse, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SKETCHWALK_H */

@@ -1,0 +1,266 @@
+// C ABI of the sketch-and-walk library: host-side validation, layout
+// computation and dispatch to the kernel launchers. Nothing here touches the
+// GPU before every argument has been checked.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <string>
+
+#include "sw_common.h"
+#include "sw_internal.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+int ok() {
+  g_err.clear();
+  return SW_OK;
+}
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+bool is_pow2(int x) { return x > 0 && (x & (x - 1)) == 0; }
+
+int check_ptr(const void* p, size_t align, const char* name) {
+  if (p == nullptr) return fail(SW_ERR_INVALID_ARG, "%s is NULL", name);
+  if (!aligned(p, align)) return fail(SW_ERR_INVALID_ARG, "%s is not %zu-byte aligned", name, align);
+  return SW_OK;
+}
+
+#define CHECK(x)              \
+  do {                        \
+    int rc_ = (x);            \
+    if (rc_ != SW_OK) return rc_; \
+  } while (0)
+
+// Builds the per-call sequence layout from host cu_seqlens.
+int build_meta(int n_seqs, const int32_t* cu, int B, sw::SeqMeta* m, int64_t* nb, int64_t* nm) {
+  if (n_seqs < 1 || n_seqs > SW_MAX_SEQS)
+    return fail(SW_ERR_INVALID_ARG, "n_seqs=%d outside [1, %d]", n_seqs, SW_MAX_SEQS);
+  if (cu == nullptr) return fail(SW_ERR_INVALID_ARG, "cu_seqlens is NULL");
+  if (B < 16 || B > 1024 || B % 16 != 0)
+    return fail(SW_ERR_INVALID_ARG, "B=%d must be a multiple of 16 in [16, 1024]", B);
+  if (cu[0] != 0) return fail(SW_ERR_INVALID_ARG, "cu_seqlens[0]=%d must be 0", cu[0]);
+  memset(m, 0, sizeof(*m));
+  m->n_seqs = n_seqs;
+  m->B = B;
+  int64_t blocks = 0, mat = 0;
+  int max_b = 0;
+  for (int s = 0; s < n_seqs; ++s) {
+    const int64_t len = (int64_t)cu[s + 1] - cu[s];
+    if (len < 1) return fail(SW_ERR_INVALID_ARG, "sequence %d has length %lld < 1", s, (long long)len);
+    const int64_t b = (len + B - 1) / B;
+    if (b > SW_MAX_BLOCKS)
+      return fail(SW_ERR_UNSUPPORTED, "sequence %d has %lld blocks > %d", s, (long long)b, SW_MAX_BLOCKS);
+    m->tok_start[s] = cu[s];
+    m->blk_start[s] = (int)blocks;
+    m->mat_start[s] = mat;
+    blocks += b;
+    mat += b * b;
+    if (b > max_b) max_b = (int)b;
+  }
+  if ((int64_t)cu[n_seqs] >= (int64_t)1 << 31)
+    return fail(SW_ERR_INVALID_ARG, "total tokens too large");
+  m->tok_start[n_seqs] = cu[n_seqs];
+  m->blk_start[n_seqs] = (int)blocks;
+  m->mat_start[n_seqs] = mat;
+  m->max_b = max_b;
+  *nb = blocks;
+  *nm = mat;
+  return SW_OK;
+}
+
+int check_heads(int h_q, int h_kv) {
+  if (h_q < 1 || h_kv < 1 || h_q % h_kv != 0)
+    return fail(SW_ERR_INVALID_ARG, "h_q=%d must be a positive multiple of h_kv=%d", h_q, h_kv);
+  if (h_q > 1024) return fail(SW_ERR_INVALID_ARG, "h_q=%d too large", h_q);
+  return SW_OK;
+}
+
+int budget(int avail, int nf, int k, int pct) {
+  int t = (k > 0) ? k : (avail * pct + 99) / 100;
+  if (t < nf) t = nf;
+  if (t > avail) t = avail;
+  return t;
+}
+
+int max_count(const sw::SeqMeta& m, int k, int pct, uint32_t flags) {
+  int best = 0;
+  for (int s = 0; s < m.n_seqs; ++s) {
+    const int b = m.blk_start[s + 1] - m.blk_start[s];
+    for (int i = 0; i < b; ++i) {
+      const int first = (flags & SW_FORCE_FIRST) ? 0 : -1;
+      const int last = (flags & SW_FORCE_LAST) ? i : -1;
+      const int nf = (first >= 0) + (last >= 0 && last != first);
+      const int t = budget(i + 1, nf, k, pct);
+      if (t > best) best = t;
+    }
+  }
+  return best;
+}
+
+int check_budget_args(int k, int density_pct, uint32_t flags) {
+  if (flags & ~(SW_FORCE_FIRST | SW_FORCE_LAST))
+    return fail(SW_ERR_INVALID_ARG, "unknown flags 0x%x", flags);
+  if (k <= 0 && (density_pct < 1 || density_pct > 100))
+    return fail(SW_ERR_INVALID_ARG, "density_pct=%d outside [1, 100] (k=%d)", density_pct, k);
+  return SW_OK;
+}
+
+int hip_status(hipError_t e, const char* what) {
+  if (e != hipSuccess) return fail(SW_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+  return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* sw_last_error(void) { return g_err.c_str(); }
+
+int sw_abi_version(void) { return SW_ABI_VERSION; }
+
+int sw_layout(int n_seqs, const int32_t* cu_seqlens, int B, int64_t* nb, int64_t* nm,
+              int32_t* max_b) {
+  sw::SeqMeta m;
+  int64_t b = 0, mm = 0;
+  CHECK(build_meta(n_seqs, cu_seqlens, B, &m, &b, &mm));
+  if (nb) *nb = b;
+  if (nm) *nm = mm;
+  if (max_b) *max_b = m.max_b;
+  return ok();
+}
+
+int64_t sw_sketch_workspace_bytes(int h_q, int h_kv, int d, int n_seqs, const int32_t* cu_seqlens,
+                                  int B) {
+  sw::SeqMeta m;
+  int64_t nb = 0, nm = 0;
+  if (build_meta(n_seqs, cu_seqlens, B, &m, &nb, &nm) != SW_OK) return -1;
+  if (check_heads(h_q, h_kv) != SW_OK) return -1;
+  if (!is_pow2(d) || d < 16 || d > 256) {
+    fail(SW_ERR_INVALID_ARG, "d=%d must be a power of two in [16, 256]", d);
+    return -1;
+  }
+  ok();
+  return sw::sketch_workspace_bytes(h_q, h_kv, d, nb);
+}
+
+int sw_select_max_count(int n_seqs, const int32_t* cu_seqlens, int B, int k, int density_pct,
+                        uint32_t flags, int32_t* kmax) {
+  sw::SeqMeta m;
+  int64_t nb = 0, nm = 0;
+  CHECK(build_meta(n_seqs, cu_seqlens, B, &m, &nb, &nm));
+  CHECK(check_budget_args(k, density_pct, flags));
+  if (kmax == nullptr) return fail(SW_ERR_INVALID_ARG, "kmax is NULL");
+  *kmax = max_count(m, k, density_pct, flags);
+  return ok();
+}
+
+int sw_sketch_scores(int dtype, const void* Q, const void* K, int h_q, int h_kv, int d,
+                     int n_seqs, const int32_t* cu_seqlens, int B, const int8_t* signs,
+                     const int32_t* cols, int r, double* Qs, double* Ks, double* A,
+                     double* A_scale, double* Qbar, double* Kbar, void* workspace,
+                     int64_t workspace_bytes, void* stream) {
+  if (dtype != SW_F32 && dtype != SW_BF16) return fail(SW_ERR_INVALID_ARG, "dtype=%d", dtype);
+  CHECK(check_heads(h_q, h_kv));
+  if (!is_pow2(d) || d < 16 || d > 256)
+    return fail(SW_ERR_INVALID_ARG, "d=%d must be a power of two in [16, 256]", d);
+  if (r < 1 || r > d) return fail(SW_ERR_INVALID_ARG, "r=%d outside [1, d=%d]", r, d);
+  sw::SeqMeta m;
+  int64_t nb = 0, nm = 0;
+  CHECK(build_meta(n_seqs, cu_seqlens, B, &m, &nb, &nm));
+  CHECK(check_ptr(Q, 16, "Q"));
+  CHECK(check_ptr(K, 16, "K"));
+  CHECK(check_ptr(signs, 1, "signs"));
+  CHECK(check_ptr(cols, 4, "cols"));
+  CHECK(check_ptr(Qs, 8, "Qs"));
+  CHECK(check_ptr(Ks, 8, "Ks"));
+  CHECK(check_ptr(A, 8, "A"));
+  CHECK(check_ptr(A_scale, 8, "A_scale"));
+  if (Qbar && !aligned(Qbar, 8)) return fail(SW_ERR_INVALID_ARG, "Qbar misaligned");
+  if (Kbar && !aligned(Kbar, 8)) return fail(SW_ERR_INVALID_ARG, "Kbar misaligned");
+  const int64_t need = sw::sketch_workspace_bytes(h_q, h_kv, d, nb);
+  CHECK(check_ptr(workspace, 256, "workspace"));
+  if (workspace_bytes < need)
+    return fail(SW_ERR_INVALID_ARG, "workspace_bytes=%lld < required %lld",
+                (long long)workspace_bytes, (long long)need);
+  hipError_t e = sw::launch_sketch(dtype, Q, K, h_q, h_kv, d, m, nb, (long long)cu_seqlens[n_seqs],
+                                   signs, cols, r, Qs, Ks, A, A_scale, Qbar, Kbar, workspace,
+                                   reinterpret_cast<hipStream_t>(stream));
+  return hip_status(e, "sw_sketch_scores launch");
+}
+
+int sw_walk_update(const double* A, const double* A_scale, int s, int n_seqs,
+                   const int32_t* cu_seqlens, int B, const double* R_prev, double* R_out,
+                   void* stream) {
+  if (s < 1 || s > 64) return fail(SW_ERR_INVALID_ARG, "s=%d outside [1, 64]", s);
+  sw::SeqMeta m;
+  int64_t nb = 0, nm = 0;
+  CHECK(build_meta(n_seqs, cu_seqlens, B, &m, &nb, &nm));
+  CHECK(check_ptr(A, 8, "A"));
+  CHECK(check_ptr(A_scale, 8, "A_scale"));
+  CHECK(check_ptr(R_out, 8, "R_out"));
+  if (R_prev && !aligned(R_prev, 8)) return fail(SW_ERR_INVALID_ARG, "R_prev misaligned");
+  if (R_out == R_prev || R_out == A) return fail(SW_ERR_INVALID_ARG, "R_out aliases an input");
+  hipError_t e = sw::launch_walk(A, A_scale, s, m, nb, R_prev, R_out,
+                                 reinterpret_cast<hipStream_t>(stream));
+  return hip_status(e, "sw_walk_update launch");
+}
+
+int sw_select_topk_blocks(const double* R, int n_seqs, const int32_t* cu_seqlens, int B, int k,
+                          int density_pct, uint32_t flags, int32_t* idx, int32_t* cnt, int kmax,
+                          void* stream) {
+  sw::SeqMeta m;
+  int64_t nb = 0, nm = 0;
+  CHECK(build_meta(n_seqs, cu_seqlens, B, &m, &nb, &nm));
+  CHECK(check_budget_args(k, density_pct, flags));
+  CHECK(check_ptr(R, 8, "R"));
+  CHECK(check_ptr(idx, 4, "idx"));
+  CHECK(check_ptr(cnt, 4, "cnt"));
+  const int need = max_count(m, k, density_pct, flags);
+  if (kmax < need) return fail(SW_ERR_INVALID_ARG, "kmax=%d < largest budget %d", kmax, need);
+  hipError_t e = sw::launch_select(R, m, nb, k, density_pct, flags, idx, cnt, kmax,
+                                   reinterpret_cast<hipStream_t>(stream));
+  return hip_status(e, "sw_select_topk_blocks launch");
+}
+
+int sw_sparse_attn_prefill(int dtype, const void* Q, const void* K, const void* V, int h_q,
+                           int h_kv, int d, int n_seqs, const int32_t* cu_seqlens, int B,
+                           const int32_t* idx, const int32_t* cnt, int kmax, float scale, void* O,
+                           float* lse, void* stream) {
+  if (dtype != SW_F32 && dtype != SW_BF16) return fail(SW_ERR_INVALID_ARG, "dtype=%d", dtype);
+  CHECK(check_heads(h_q, h_kv));
+  if (d != 64 && d != 128) return fail(SW_ERR_UNSUPPORTED, "attention head dim d=%d (64 or 128)", d);
+  if (B != 64 && B != 128) return fail(SW_ERR_UNSUPPORTED, "attention block size B=%d (64 or 128)", B);
+  sw::SeqMeta m;
+  int64_t nb = 0, nm = 0;
+  CHECK(build_meta(n_seqs, cu_seqlens, B, &m, &nb, &nm));
+  CHECK(check_ptr(Q, 16, "Q"));
+  CHECK(check_ptr(K, 16, "K"));
+  CHECK(check_ptr(V, 16, "V"));
+  CHECK(check_ptr(O, 16, "O"));
+  CHECK(check_ptr(idx, 4, "idx"));
+  CHECK(check_ptr(cnt, 4, "cnt"));
+  if (lse && !aligned(lse, 4)) return fail(SW_ERR_INVALID_ARG, "lse misaligned");
+  if (kmax < 1) return fail(SW_ERR_INVALID_ARG, "kmax=%d < 1", kmax);
+  if (!(scale > 0.0f)) scale = 1.0f / sqrtf((float)d);
+  hipError_t e = sw::launch_attn_prefill(dtype, Q, K, V, h_q, h_kv, d,
+                                         (long long)cu_seqlens[n_seqs], m, nb, idx, cnt, kmax,
+                                         scale, O, lse, reinterpret_cast<hipStream_t>(stream));
+  return hip_status(e, "sw_sparse_attn_prefill launch");
+}
+
+}  // extern "C"

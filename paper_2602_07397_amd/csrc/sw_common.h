@@ -1,0 +1,82 @@
+// Shared device/host helpers for the sketch-and-walk HIP library (gfx950).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/sketchwalk.h"
+
+namespace sw {
+
+// Lane layouts of the matrix instructions used here (measured on gfx950):
+//  v_mfma_f64_16x16x4f64: A[m][k] from lane m + 16k, B[k][n] from lane n + 16k,
+//    D[m][n] in lane n + 16 (m % 4), element m / 4.
+//  v_mfma_f32_32x32x16_bf16 / v_mfma_f32_32x32x2f32: A[m][k] from lane
+//    m + 32 (k / K_lane), element k % K_lane (K_lane = 8 / 1), B[k][n] from lane
+//    n + 32 (k / K_lane); D[m][n] in lane n + 32 ((m / 4) % 2), element
+//    4 (m / 8) + m % 4.
+
+// Per-call sequence layout, passed to kernels by value (fits the kernel
+// argument space for up to SW_MAX_SEQS sequences).
+struct SeqMeta {
+  int n_seqs;
+  int B;
+  int max_b;                              // largest per-sequence block count
+  int tok_start[SW_MAX_SEQS + 1];         // cu_seqlens
+  int blk_start[SW_MAX_SEQS + 1];         // prefix sums of b_s = ceil(n_s / B)
+  long long mat_start[SW_MAX_SEQS + 1];   // prefix sums of b_s * b_s
+  int aux_start[SW_MAX_SEQS + 1];         // per-launch prefix (e.g. tile counts)
+};
+
+// Sequence that owns global block row `row` (blk_start is increasing).
+__device__ __forceinline__ int seq_of_block(const SeqMeta& m, int row) {
+  int lo = 0, hi = m.n_seqs - 1;
+  while (lo < hi) {
+    int mid = (lo + hi + 1) >> 1;
+    if (m.blk_start[mid] <= row) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t h) {
+  return __uint_as_float(((uint32_t)h) << 16);
+}
+
+// Round-to-nearest-even fp32 -> bf16 (inputs are finite).
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return (uint32_t)f32_to_bf16(lo) | ((uint32_t)f32_to_bf16(hi) << 16);
+}
+
+// Monotone map from a double to uint64 (larger double -> larger key);
+// -0.0 is folded onto +0.0 so that equal values compare equal.
+__device__ __forceinline__ unsigned long long order_key(double v) {
+  v = v + 0.0;
+  unsigned long long u = (unsigned long long)__double_as_longlong(v);
+  return (u >> 63) ? ~u : (u | 0x8000000000000000ull);
+}
+
+// Exclusive prefix sum over a 256-thread block. `tmp` holds 256 ints of LDS.
+// Returns the exclusive prefix of `v`; `*total` receives the block sum.
+__device__ __forceinline__ int block_exclusive_scan_256(int v, int* tmp, int* total) {
+  const int t = threadIdx.x;
+  tmp[t] = v;
+  __syncthreads();
+  for (int off = 1; off < 256; off <<= 1) {
+    int add = (t >= off) ? tmp[t - off] : 0;
+    __syncthreads();
+    tmp[t] += add;
+    __syncthreads();
+  }
+  int incl = tmp[t];
+  *total = tmp[255];
+  __syncthreads();
+  return incl - v;
+}
+
+}  // namespace sw

@@ -1,0 +1,125 @@
+"""CPU checks of the C ABI: the library loads, exports every function the
+public header declares, and rejects invalid arguments on the host before any
+GPU work (no compute call is made here)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2602_07397_amd import binding as sw
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "sketchwalk.h")
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(sw_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_library_loads_and_reports_version():
+    lib = sw.load()
+    assert lib.sw_abi_version() == 1
+
+
+def test_every_declared_function_is_exported_and_bound():
+    lib = sw.load()
+    names = _declared_functions()
+    assert len(names) >= 9
+    for name in names:
+        assert hasattr(lib, name), name
+        assert name in sw.exported_symbols(), f"{name} missing from the binding"
+
+
+def test_layout_and_budget_queries():
+    assert sw.layout([0, 2048], 64) == (32, 1024, 32)
+    assert sw.layout(np.cumsum([0, 100, 300, 64]), 64) == (2 + 5 + 1, 4 + 25 + 1, 5)
+    # tiny workload at 20%: largest row budget is ceil(32 * 20 / 100) = 7
+    assert sw.select_max_count([0, 2048], 64, density_pct=20) == 7
+    assert sw.select_max_count([0, 2048], 64, density_pct=100) == 32
+    assert sw.select_max_count([0, 2048], 64, k=3, flags=0) == 3
+    assert sw.sketch_workspace_bytes(32, 8, 128, [0, 32768], 128) > 0
+
+
+def _err(fn, *args):
+    lib = sw.load()
+    rc = getattr(lib, fn)(*args)
+    return rc, lib.sw_last_error().decode()
+
+
+def _cu(vals):
+    arr = (ctypes.c_int32 * len(vals))(*vals)
+    return arr
+
+
+FAKE = 1 << 20   # 16-byte aligned non-null address; never dereferenced
+
+
+def test_sketch_rejects_bad_arguments():
+    cu = _cu([0, 256])
+    base = [sw.SW_BF16, FAKE, FAKE, 4, 2, 64, 1, cu, 64, FAKE, FAKE, 32,
+            FAKE, FAKE, FAKE, FAKE, None, None, FAKE, 1 << 30, None]
+    # every case below must fail host validation: nothing is ever launched
+    cases = {
+        "dtype": (0, 7),
+        "heads": (4, 3),          # h_q=4 not a multiple of h_kv=3
+        "d": (5, 48),             # not a power of two
+        "r": (11, 65),            # r > d
+        "B": (8, 24),             # not a multiple of 16
+        "nseq": (6, 0),
+        "Q null": (1, None),
+        "Q misaligned": (1, FAKE + 2),
+        "ws small": (19, 16),
+    }
+    for name, (pos, val) in cases.items():
+        args = list(base)
+        args[pos] = val
+        rc, msg = _err("sw_sketch_scores", *args)
+        assert rc == 1, (name, rc, msg)
+        assert msg, name
+
+
+def test_sketch_rejects_bad_cu_seqlens():
+    args = [sw.SW_BF16, FAKE, FAKE, 4, 2, 64, 2, _cu([0, 100, 100]), 64, FAKE, FAKE, 32,
+            FAKE, FAKE, FAKE, FAKE, None, None, FAKE, 1 << 30, None]
+    rc, msg = _err("sw_sketch_scores", *args)
+    assert rc == 1 and "length" in msg
+    args[7] = _cu([5, 100, 200])
+    rc, msg = _err("sw_sketch_scores", *args)
+    assert rc == 1
+
+
+def test_walk_select_attention_reject_bad_arguments():
+    cu = _cu([0, 256])
+    rc, msg = _err("sw_walk_update", FAKE, FAKE, 0, 1, cu, 64, None, FAKE + 256, None)
+    assert rc == 1 and "s=" in msg
+    rc, msg = _err("sw_walk_update", FAKE, FAKE, 8, 1, cu, 64, FAKE, FAKE, None)
+    assert rc == 1 and "alias" in msg
+    # kmax below the largest budget
+    rc, msg = _err("sw_select_topk_blocks", FAKE, 1, cu, 64, 0, 50, 3, FAKE, FAKE, 1, None)
+    assert rc == 1 and "kmax" in msg
+    rc, msg = _err("sw_select_topk_blocks", FAKE, 1, cu, 64, 0, 0, 3, FAKE, FAKE, 8, None)
+    assert rc == 1 and "density" in msg
+    rc, msg = _err("sw_select_topk_blocks", FAKE, 1, cu, 64, 0, 20, 8, FAKE, FAKE, 8, None)
+    assert rc == 1 and "flags" in msg
+    # attention: unsupported head dim / block size
+    rc, msg = _err("sw_sparse_attn_prefill", sw.SW_BF16, FAKE, FAKE, FAKE, 4, 2, 96, 1, cu, 64,
+                   FAKE, FAKE, 4, ctypes.c_float(0.0), FAKE, None, None)
+    assert rc == 2
+    rc, msg = _err("sw_sparse_attn_prefill", sw.SW_BF16, FAKE, FAKE, FAKE, 4, 2, 128, 1, cu, 32,
+                   FAKE, FAKE, 4, ctypes.c_float(0.0), FAKE, None, None)
+    assert rc == 2
+    rc, msg = _err("sw_sparse_attn_prefill", sw.SW_BF16, FAKE, FAKE, FAKE, 4, 3, 128, 1, cu, 64,
+                   FAKE, FAKE, 4, ctypes.c_float(0.0), FAKE, None, None)
+    assert rc == 1
+
+
+def test_binding_refuses_cpu_tensors():
+    import torch
+    x = torch.zeros((1, 64, 64))
+    with pytest.raises(sw.SketchWalkError):
+        sw.sparse_attn_prefill(x, x, x, [0, 64], 64, torch.zeros((1, 1), dtype=torch.int32),
+                               torch.zeros(1, dtype=torch.int32), 1)
