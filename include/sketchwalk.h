@@ -171,6 +171,107 @@ int sw_sparse_attn_prefill(int dtype, const void* Q, const void* K, const void* 
                            const int32_t* idx, const int32_t* cnt, int kmax, float scale,
                            void* O, float* lse, void* stream);
 
+/* ======================================================================
+ * Decode (paper Alg. 2): one new token per sequence per layer.
+ *
+ * Per-layer decode state: one caller-owned device buffer of
+ * sw_decode_state_bytes(batch, d, r, b_max) bytes (256-byte aligned), laid
+ * out as consecutive 256-byte-aligned sections
+ *   double A_scale[batch]         score scale c (frozen at its prefill value)
+ *   int32  col0[batch]            first key block whose column decode fills
+ *                                 (= prompt length / B)
+ *   int32  cnt[batch][2]          token counts of the open query / key block
+ *   double bar[batch][2][d]       running means of the open query / key block
+ *   double Qs[batch][b_max][r]    sketch of every query-block representative
+ *   double Ks[batch][b_max][r]    sketch of every key-block representative
+ *   float  A[batch][b_max][b_max] block-score cache (fp32)
+ * Checkpointing a decode is a byte copy of this buffer (plus the caches).
+ * pos [batch] int32 (device): 0-based position of the new token of each
+ * sequence; b_cur = pos / B is the open block. Sequences whose pos is
+ * negative, >= T_max (attention, append) or beyond b_max blocks are skipped:
+ * their outputs are left untouched.
+ * ====================================================================== */
+
+/* Host-only: bytes of one layer's decode state (-1 on invalid arguments). */
+int64_t sw_decode_state_bytes(int batch, int d, int r, int b_max);
+
+/* Fills sequence `seq` of a layer's decode state from the prefill sketch of
+   its n-token prompt (one sequence's outputs of sw_sketch_scores: Qs, Ks
+   [b][r], A [b][b], A_scale [1], Qbar, Kbar [b][d], b = ceil(n/B) <= b_max).
+   The open block is the prompt's last block (with its token count); the
+   score cache is zero outside the prompt's b x b corner. Alg. 2 inputs: the
+   cached block reps and block-score estimate from prefill. */
+int sw_decode_state_init(void* state, int batch, int d, int r, int b_max, int seq, int n, int B,
+                         const double* Qs, const double* Ks, const double* A,
+                         const double* A_scale, const double* Qbar, const double* Kbar,
+                         void* stream);
+
+/* Alg. 2 step 1: writes k_new, v_new [batch][h_kv][d] into the caches
+   Kc, Vc [batch][h_kv][T_max][d] at token pos[b]. */
+int sw_kv_append(int dtype, const void* k_new, const void* v_new, void* Kc, void* Vc, int batch,
+                 int h_kv, int d, int T_max, const int32_t* pos, void* stream);
+
+/*
+ * sw_sketch_scores_decode - Alg. 2 steps 2-4 for the tokens q_new
+ * [batch][h_q][d], k_new [batch][h_kv][d] at pos[b]:
+ *   - running mean of the head-averaged key (and query) of the open block
+ *     (restarted when pos % B == 0);
+ *   - q~_t = SRHT(head-averaged query), and the sketches of both open
+ *     representatives (stored in Qs[b_cur], Ks[b_cur]);
+ *   - (i) new query row A[b_cur][j] = q~_t . Ks[j] / sqrt(r), j < b_cur;
+ *     (ii) last column A[m][b_cur] = Qs[m] . Ks[b_cur] / sqrt(r), m <= b_cur
+ *     (the diagonal entry comes from (ii)).
+ * signs/cols/r as in sw_sketch_scores (same transform as the prompt).
+ */
+int sw_sketch_scores_decode(int dtype, const void* q_new, const void* k_new, int batch, int h_q,
+                            int h_kv, int d, int B, const int32_t* pos, const int8_t* signs,
+                            const int32_t* cols, int r, int b_max, void* state, void* stream);
+
+/* Host-only: workspace bytes of sw_walk_update_decode (-1 on bad input). */
+int64_t sw_walk_decode_workspace_bytes(int batch, int b_max);
+
+/*
+ * sw_walk_update_decode - Alg. 2 step 5 on the current query row:
+ *   r_out = W[b_cur, :] if r_prev is NULL (first walked layer), else
+ *   r_prev W, with W = (A / c)^s element-wise over the layer's score cache;
+ *   then divided by its largest magnitude. r_prev, r_out [batch][b_max]
+ *   float64 (entries past b_cur are written as 0); the workspace is needed
+ *   when r_prev is given. Sums run in fp64 in a fixed order.
+ */
+int sw_walk_update_decode(const void* state, int batch, int d, int r, int b_max, int B,
+                          const int32_t* pos, int s, const double* r_prev, double* r_out,
+                          void* workspace, int64_t workspace_bytes, void* stream);
+
+/* Host-only: the largest decode budget over rows of up to b_max blocks. */
+int sw_select_max_count_decode(int b_max, int k, int density_pct, uint32_t flags, int32_t* kmax);
+
+/*
+ * sw_select_topk_blocks_decode - Alg. 2 step 6: per sequence, key blocks
+ * 0..b_cur ranked by the walk row rows[b] (from sw_walk_update_decode); the
+ * forced set is {0 (SW_FORCE_FIRST), b_cur (SW_FORCE_LAST)} and counts
+ * inside tau = ceil((b_cur+1) density_pct / 100) (or k). idx [batch][kmax]
+ * ascending, -1 padded; cnt [batch].
+ */
+int sw_select_topk_blocks_decode(const double* rows, int batch, int b_max, int B,
+                                 const int32_t* pos, int k, int density_pct, uint32_t flags,
+                                 int32_t* idx, int32_t* cnt, int kmax, void* stream);
+
+/* Host-only: workspace bytes of sw_sparse_attn_decode (-1 on bad input). */
+int64_t sw_decode_attn_workspace_bytes(int batch, int h_q, int h_kv, int d);
+
+/*
+ * sw_sparse_attn_decode - Alg. 2 step 7: for each sequence b and query head
+ * u (g = u / G), softmax(scale q[b][u] . Kc[b][g][t]) over the tokens
+ * t <= pos[b] of the selected blocks, applied to Vc. Split-K over the
+ * selected tokens with a log-sum-exp merge. q [batch][h_q][d]; Kc, Vc
+ * [batch][h_kv][T_max][d]; O [batch][h_q][d] in the input dtype.
+ * G = h_q / h_kv in {1, 2, 4, 8}; d in {64, 128}; scale <= 0 -> 1/sqrt(d).
+ */
+int sw_sparse_attn_decode(int dtype, const void* q, const void* Kc, const void* Vc, int batch,
+                          int h_q, int h_kv, int d, int T_max, int B, const int32_t* pos,
+                          const int32_t* idx, const int32_t* cnt, int kmax, float scale, void* O,
+                          void* workspace, int64_t workspace_bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

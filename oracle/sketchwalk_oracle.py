@@ -56,6 +56,7 @@ design notes of the repository):
 from __future__ import annotations
 
 import dataclasses
+import functools
 import math
 from typing import List, Optional, Sequence, Tuple
 
@@ -120,15 +121,18 @@ def block_means(Xa: np.ndarray, B: int) -> np.ndarray:
     return out
 
 
+@functools.lru_cache(maxsize=None)
 def sylvester_hadamard(d: int) -> np.ndarray:
     """The d x d Walsh-Hadamard matrix in natural (Sylvester) order:
-    entry (a, m) is (-1) ** popcount(a & m). d must be a power of two."""
+    entry (a, m) is (-1) ** popcount(a & m). d must be a power of two.
+    (Cached; the returned array is read-only.)"""
     if d < 1 or (d & (d - 1)) != 0:
         raise ValueError("d must be a power of two")
     H = np.empty((d, d), dtype=np.float64)
     for a in range(d):
         for m in range(d):
             H[a, m] = -1.0 if bin(a & m).count("1") % 2 else 1.0
+    H.setflags(write=False)
     return H
 
 

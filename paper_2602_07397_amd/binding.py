@@ -47,6 +47,22 @@ _SIGNATURES = {
                                        _vp, _vp, _c_int, _vp]),
     "sw_sparse_attn_prefill": (_c_int, [_c_int, _vp, _vp, _vp, _c_int, _c_int, _c_int, _c_int, _i32p,
                                         _c_int, _vp, _vp, _c_int, ctypes.c_float, _vp, _vp, _vp]),
+    "sw_decode_state_bytes": (_c_i64, [_c_int, _c_int, _c_int, _c_int]),
+    "sw_decode_state_init": (_c_int, [_vp, _c_int, _c_int, _c_int, _c_int, _c_int, _c_int, _c_int,
+                                      _vp, _vp, _vp, _vp, _vp, _vp, _vp]),
+    "sw_kv_append": (_c_int, [_c_int, _vp, _vp, _vp, _vp, _c_int, _c_int, _c_int, _c_int, _vp, _vp]),
+    "sw_sketch_scores_decode": (_c_int, [_c_int, _vp, _vp, _c_int, _c_int, _c_int, _c_int, _c_int, _vp,
+                                         _vp, _vp, _c_int, _c_int, _vp, _vp]),
+    "sw_walk_decode_workspace_bytes": (_c_i64, [_c_int, _c_int]),
+    "sw_walk_update_decode": (_c_int, [_vp, _c_int, _c_int, _c_int, _c_int, _c_int, _vp, _c_int, _vp,
+                                       _vp, _vp, _c_i64, _vp]),
+    "sw_select_max_count_decode": (_c_int, [_c_int, _c_int, _c_int, ctypes.c_uint32, _i32p]),
+    "sw_select_topk_blocks_decode": (_c_int, [_vp, _c_int, _c_int, _c_int, _vp, _c_int, _c_int,
+                                              ctypes.c_uint32, _vp, _vp, _c_int, _vp]),
+    "sw_decode_attn_workspace_bytes": (_c_i64, [_c_int, _c_int, _c_int, _c_int]),
+    "sw_sparse_attn_decode": (_c_int, [_c_int, _vp, _vp, _vp, _c_int, _c_int, _c_int, _c_int, _c_int,
+                                       _c_int, _vp, _vp, _vp, _c_int, ctypes.c_float, _vp, _vp, _c_i64,
+                                       _vp]),
 }
 
 _lib = None
@@ -235,3 +251,137 @@ def sparse_attn_prefill(Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, cu_se
                                     _stream(Q.device))
     _check(rc, "sw_sparse_attn_prefill")
     return (O, lse) if want_lse else O
+
+
+# ---------------------------------------------------------------------------
+# decode (Alg. 2)
+# ---------------------------------------------------------------------------
+
+def decode_state_bytes(batch: int, d: int, r: int, b_max: int) -> int:
+    v = load().sw_decode_state_bytes(batch, d, r, b_max)
+    if v < 0:
+        _check(1, "sw_decode_state_bytes")
+    return int(v)
+
+
+def new_decode_state(batch: int, d: int, r: int, b_max: int, device) -> torch.Tensor:
+    """A zero-filled byte buffer holding one layer's decode state."""
+    return torch.zeros((decode_state_bytes(batch, d, r, b_max),), dtype=torch.uint8, device=device)
+
+
+def decode_state_init(state: torch.Tensor, batch: int, d: int, r: int, b_max: int, seq: int, n: int,
+                      B: int, sk: dict) -> None:
+    """Initialises sequence ``seq`` of ``state`` from one sequence's
+    sketch_scores output (computed with want_means=True)."""
+    rc = load().sw_decode_state_init(
+        _dev(state, "state", torch.uint8), batch, d, r, b_max, seq, n, B,
+        _dev(sk["Qs"], "Qs", torch.float64), _dev(sk["Ks"], "Ks", torch.float64),
+        _dev(sk["A"], "A", torch.float64), _dev(sk["A_scale"], "A_scale", torch.float64),
+        _dev(sk["Qbar"], "Qbar", torch.float64), _dev(sk["Kbar"], "Kbar", torch.float64),
+        _stream(state.device))
+    _check(rc, "sw_decode_state_init")
+
+
+def kv_append(k_new: torch.Tensor, v_new: torch.Tensor, Kc: torch.Tensor, Vc: torch.Tensor,
+              pos: torch.Tensor) -> None:
+    batch, h_kv, T_max, d = Kc.shape
+    rc = load().sw_kv_append(_dtype_code(Kc), _dev(k_new, "k_new", Kc.dtype), _dev(v_new, "v_new", Kc.dtype),
+                             _dev(Kc, "Kc"), _dev(Vc, "Vc", Kc.dtype), batch, h_kv, d, T_max,
+                             _dev(pos, "pos", torch.int32), _stream(Kc.device))
+    _check(rc, "sw_kv_append")
+
+
+def sketch_scores_decode(q_new: torch.Tensor, k_new: torch.Tensor, B: int, pos: torch.Tensor,
+                         signs: torch.Tensor, cols: torch.Tensor, b_max: int,
+                         state: torch.Tensor) -> None:
+    batch, h_q, d = q_new.shape
+    h_kv = k_new.shape[1]
+    rc = load().sw_sketch_scores_decode(
+        _dtype_code(q_new), _dev(q_new, "q_new"), _dev(k_new, "k_new", q_new.dtype), batch, h_q, h_kv,
+        d, B, _dev(pos, "pos", torch.int32), _dev(signs, "signs", torch.int8),
+        _dev(cols, "cols", torch.int32), int(cols.numel()), b_max, _dev(state, "state", torch.uint8),
+        _stream(q_new.device))
+    _check(rc, "sw_sketch_scores_decode")
+
+
+def walk_decode_workspace_bytes(batch: int, b_max: int) -> int:
+    v = load().sw_walk_decode_workspace_bytes(batch, b_max)
+    if v < 0:
+        _check(1, "sw_walk_decode_workspace_bytes")
+    return int(v)
+
+
+def walk_update_decode(state: torch.Tensor, batch: int, d: int, r: int, b_max: int, B: int,
+                       pos: torch.Tensor, s: int, r_prev: Optional[torch.Tensor] = None,
+                       r_out: Optional[torch.Tensor] = None,
+                       workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
+    dev = state.device
+    if r_out is None:
+        r_out = torch.empty((batch, b_max), dtype=torch.float64, device=dev)
+    wsb = walk_decode_workspace_bytes(batch, b_max)
+    if workspace is None or workspace.numel() < wsb:
+        workspace = torch.empty((wsb,), dtype=torch.uint8, device=dev)
+    rc = load().sw_walk_update_decode(_dev(state, "state", torch.uint8), batch, d, r, b_max, B,
+                                      _dev(pos, "pos", torch.int32), s,
+                                      _opt(r_prev, "r_prev", torch.float64),
+                                      _dev(r_out, "r_out", torch.float64), _dev(workspace, "workspace"),
+                                      workspace.numel(), _stream(dev))
+    _check(rc, "sw_walk_update_decode")
+    return r_out
+
+
+def select_max_count_decode(b_max: int, k: int = 0, density_pct: int = 20,
+                            flags: int = FORCE_BOTH) -> int:
+    out = ctypes.c_int32()
+    _check(load().sw_select_max_count_decode(b_max, k, density_pct, flags, ctypes.byref(out)),
+           "sw_select_max_count_decode")
+    return out.value
+
+
+def select_topk_blocks_decode(rows: torch.Tensor, B: int, pos: torch.Tensor, k: int = 0,
+                              density_pct: int = 20, flags: int = FORCE_BOTH,
+                              kmax: Optional[int] = None, idx: Optional[torch.Tensor] = None,
+                              cnt: Optional[torch.Tensor] = None):
+    batch, b_max = rows.shape
+    if kmax is None:
+        kmax = select_max_count_decode(b_max, k, density_pct, flags)
+    if idx is None:
+        idx = torch.empty((batch, kmax), dtype=torch.int32, device=rows.device)
+    if cnt is None:
+        cnt = torch.empty((batch,), dtype=torch.int32, device=rows.device)
+    rc = load().sw_select_topk_blocks_decode(_dev(rows, "rows", torch.float64), batch, b_max, B,
+                                             _dev(pos, "pos", torch.int32), k, density_pct, flags,
+                                             _dev(idx, "idx", torch.int32), _dev(cnt, "cnt", torch.int32),
+                                             kmax, _stream(rows.device))
+    _check(rc, "sw_select_topk_blocks_decode")
+    return idx, cnt, kmax
+
+
+def decode_attn_workspace_bytes(batch: int, h_q: int, h_kv: int, d: int) -> int:
+    v = load().sw_decode_attn_workspace_bytes(batch, h_q, h_kv, d)
+    if v < 0:
+        _check(1, "sw_decode_attn_workspace_bytes")
+    return int(v)
+
+
+def sparse_attn_decode(q: torch.Tensor, Kc: torch.Tensor, Vc: torch.Tensor, B: int, pos: torch.Tensor,
+                       idx: torch.Tensor, cnt: torch.Tensor, kmax: int, scale: float = 0.0,
+                       O: Optional[torch.Tensor] = None,
+                       workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
+    batch, h_q, d = q.shape
+    _, h_kv, T_max, _ = Kc.shape
+    dev = q.device
+    if O is None:
+        O = torch.empty_like(q)
+    wsb = decode_attn_workspace_bytes(batch, h_q, h_kv, d)
+    if workspace is None or workspace.numel() < wsb:
+        workspace = torch.empty((max(wsb, 256),), dtype=torch.uint8, device=dev)
+    if not (Kc.dtype == Vc.dtype == q.dtype == O.dtype):
+        raise SketchWalkError("q, Kc, Vc, O must share a dtype")
+    rc = load().sw_sparse_attn_decode(_dtype_code(q), _dev(q, "q"), _dev(Kc, "Kc"), _dev(Vc, "Vc"),
+                                      batch, h_q, h_kv, d, T_max, B, _dev(pos, "pos", torch.int32),
+                                      _dev(idx, "idx", torch.int32), _dev(cnt, "cnt", torch.int32), kmax,
+                                      float(scale), _dev(O, "O"), _dev(workspace, "workspace"),
+                                      workspace.numel(), _stream(dev))
+    _check(rc, "sw_sparse_attn_decode")
+    return O

@@ -263,4 +263,193 @@ int sw_sparse_attn_prefill(int dtype, const void* Q, const void* K, const void* 
   return hip_status(e, "sw_sparse_attn_prefill launch");
 }
 
+// ---------------------------------------------------------------------------
+// decode (Alg. 2)
+// ---------------------------------------------------------------------------
+
+static int check_decode_shape(int batch, int d, int r, int b_max, int B) {
+  if (batch < 1 || batch > 65536) return fail(SW_ERR_INVALID_ARG, "batch=%d outside [1, 65536]", batch);
+  if (!is_pow2(d) || d < 16 || d > 256)
+    return fail(SW_ERR_INVALID_ARG, "d=%d must be a power of two in [16, 256]", d);
+  if (r < 1 || r > d) return fail(SW_ERR_INVALID_ARG, "r=%d outside [1, d=%d]", r, d);
+  if (b_max < 1 || b_max > SW_MAX_BLOCKS)
+    return fail(SW_ERR_INVALID_ARG, "b_max=%d outside [1, %d]", b_max, SW_MAX_BLOCKS);
+  if (B < 16 || B > 1024 || B % 16 != 0)
+    return fail(SW_ERR_INVALID_ARG, "B=%d must be a multiple of 16 in [16, 1024]", B);
+  return SW_OK;
+}
+
+static int max_count_decode(int b_max, int k, int pct, uint32_t flags) {
+  int best = 0;
+  for (int a = 1; a <= b_max; ++a) {
+    const int first = (flags & SW_FORCE_FIRST) ? 0 : -1;
+    const int last = (flags & SW_FORCE_LAST) ? a - 1 : -1;
+    const int nf = (first >= 0) + (last >= 0 && last != first);
+    const int t = budget(a, nf, k, pct);
+    if (t > best) best = t;
+  }
+  return best;
+}
+
+int64_t sw_decode_state_bytes(int batch, int d, int r, int b_max) {
+  if (check_decode_shape(batch, d, r, b_max, 64) != SW_OK) return -1;
+  ok();
+  return sw::decode_layout(batch, d, r, b_max).total;
+}
+
+int sw_decode_state_init(void* state, int batch, int d, int r, int b_max, int seq, int n, int B,
+                         const double* Qs, const double* Ks, const double* A,
+                         const double* A_scale, const double* Qbar, const double* Kbar,
+                         void* stream) {
+  CHECK(check_decode_shape(batch, d, r, b_max, B));
+  if (seq < 0 || seq >= batch) return fail(SW_ERR_INVALID_ARG, "seq=%d outside [0, %d)", seq, batch);
+  if (n < 1 || (n + B - 1) / B > b_max)
+    return fail(SW_ERR_INVALID_ARG, "prompt length n=%d needs more than b_max=%d blocks", n, b_max);
+  CHECK(check_ptr(state, 256, "state"));
+  CHECK(check_ptr(Qs, 8, "Qs"));
+  CHECK(check_ptr(Ks, 8, "Ks"));
+  CHECK(check_ptr(A, 8, "A"));
+  CHECK(check_ptr(A_scale, 8, "A_scale"));
+  CHECK(check_ptr(Qbar, 8, "Qbar"));
+  CHECK(check_ptr(Kbar, 8, "Kbar"));
+  hipError_t e = sw::launch_decode_init(reinterpret_cast<char*>(state), batch, d, r, b_max, seq, n, B,
+                                        Qs, Ks, A, A_scale, Qbar, Kbar,
+                                        reinterpret_cast<hipStream_t>(stream));
+  return hip_status(e, "sw_decode_state_init launch");
+}
+
+int sw_kv_append(int dtype, const void* k_new, const void* v_new, void* Kc, void* Vc, int batch,
+                 int h_kv, int d, int T_max, const int32_t* pos, void* stream) {
+  if (dtype != SW_F32 && dtype != SW_BF16) return fail(SW_ERR_INVALID_ARG, "dtype=%d", dtype);
+  if (batch < 1 || h_kv < 1 || d < 1 || T_max < 1)
+    return fail(SW_ERR_INVALID_ARG, "batch=%d h_kv=%d d=%d T_max=%d must be positive", batch, h_kv, d, T_max);
+  CHECK(check_ptr(k_new, 4, "k_new"));
+  CHECK(check_ptr(v_new, 4, "v_new"));
+  CHECK(check_ptr(Kc, 4, "Kc"));
+  CHECK(check_ptr(Vc, 4, "Vc"));
+  CHECK(check_ptr(pos, 4, "pos"));
+  hipError_t e = sw::launch_kv_append(dtype, k_new, v_new, Kc, Vc, batch, h_kv, d, T_max, pos,
+                                      reinterpret_cast<hipStream_t>(stream));
+  return hip_status(e, "sw_kv_append launch");
+}
+
+int sw_sketch_scores_decode(int dtype, const void* q_new, const void* k_new, int batch, int h_q,
+                            int h_kv, int d, int B, const int32_t* pos, const int8_t* signs,
+                            const int32_t* cols, int r, int b_max, void* state, void* stream) {
+  if (dtype != SW_F32 && dtype != SW_BF16) return fail(SW_ERR_INVALID_ARG, "dtype=%d", dtype);
+  CHECK(check_heads(h_q, h_kv));
+  CHECK(check_decode_shape(batch, d, r, b_max, B));
+  CHECK(check_ptr(q_new, 4, "q_new"));
+  CHECK(check_ptr(k_new, 4, "k_new"));
+  CHECK(check_ptr(pos, 4, "pos"));
+  CHECK(check_ptr(signs, 1, "signs"));
+  CHECK(check_ptr(cols, 4, "cols"));
+  CHECK(check_ptr(state, 256, "state"));
+  hipError_t e = sw::launch_decode_sketch(dtype, q_new, k_new, batch, h_q, h_kv, d, B, pos, signs,
+                                          cols, r, b_max, reinterpret_cast<char*>(state),
+                                          reinterpret_cast<hipStream_t>(stream));
+  return hip_status(e, "sw_sketch_scores_decode launch");
+}
+
+int64_t sw_walk_decode_workspace_bytes(int batch, int b_max) {
+  if (batch < 1 || b_max < 1 || b_max > SW_MAX_BLOCKS) {
+    fail(SW_ERR_INVALID_ARG, "batch=%d b_max=%d", batch, b_max);
+    return -1;
+  }
+  ok();
+  const int64_t nch = (b_max + sw::kWalkRowChunk - 1) / sw::kWalkRowChunk;
+  return (int64_t)batch * nch * b_max * 8;
+}
+
+int sw_walk_update_decode(const void* state, int batch, int d, int r, int b_max, int B,
+                          const int32_t* pos, int s, const double* r_prev, double* r_out,
+                          void* workspace, int64_t workspace_bytes, void* stream) {
+  if (s < 1 || s > 64) return fail(SW_ERR_INVALID_ARG, "s=%d outside [1, 64]", s);
+  CHECK(check_decode_shape(batch, d, r, b_max, B));
+  CHECK(check_ptr(state, 256, "state"));
+  CHECK(check_ptr(pos, 4, "pos"));
+  CHECK(check_ptr(r_out, 8, "r_out"));
+  if (r_prev && !aligned(r_prev, 8)) return fail(SW_ERR_INVALID_ARG, "r_prev misaligned");
+  if (r_prev == r_out) return fail(SW_ERR_INVALID_ARG, "r_out aliases r_prev");
+  if (r_prev) {
+    const int64_t need = sw_walk_decode_workspace_bytes(batch, b_max);
+    CHECK(check_ptr(workspace, 256, "workspace"));
+    if (workspace_bytes < need)
+      return fail(SW_ERR_INVALID_ARG, "workspace_bytes=%lld < required %lld",
+                  (long long)workspace_bytes, (long long)need);
+  }
+  hipError_t e = sw::launch_decode_walk(reinterpret_cast<const char*>(state), batch, d, r, b_max, B,
+                                        pos, s, r_prev, r_out, reinterpret_cast<double*>(workspace),
+                                        reinterpret_cast<hipStream_t>(stream));
+  return hip_status(e, "sw_walk_update_decode launch");
+}
+
+int sw_select_max_count_decode(int b_max, int k, int density_pct, uint32_t flags, int32_t* kmax) {
+  if (b_max < 1 || b_max > SW_MAX_BLOCKS)
+    return fail(SW_ERR_INVALID_ARG, "b_max=%d outside [1, %d]", b_max, SW_MAX_BLOCKS);
+  CHECK(check_budget_args(k, density_pct, flags));
+  if (kmax == nullptr) return fail(SW_ERR_INVALID_ARG, "kmax is NULL");
+  *kmax = max_count_decode(b_max, k, density_pct, flags);
+  return ok();
+}
+
+int sw_select_topk_blocks_decode(const double* rows, int batch, int b_max, int B,
+                                 const int32_t* pos, int k, int density_pct, uint32_t flags,
+                                 int32_t* idx, int32_t* cnt, int kmax, void* stream) {
+  CHECK(check_decode_shape(batch, 16, 1, b_max, B));
+  CHECK(check_budget_args(k, density_pct, flags));
+  CHECK(check_ptr(rows, 8, "rows"));
+  CHECK(check_ptr(pos, 4, "pos"));
+  CHECK(check_ptr(idx, 4, "idx"));
+  CHECK(check_ptr(cnt, 4, "cnt"));
+  const int need = max_count_decode(b_max, k, density_pct, flags);
+  if (kmax < need) return fail(SW_ERR_INVALID_ARG, "kmax=%d < largest budget %d", kmax, need);
+  hipError_t e = sw::launch_select_decode(rows, batch, b_max, B, pos, k, density_pct, flags, idx,
+                                          cnt, kmax, reinterpret_cast<hipStream_t>(stream));
+  return hip_status(e, "sw_select_topk_blocks_decode launch");
+}
+
+int64_t sw_decode_attn_workspace_bytes(int batch, int h_q, int h_kv, int d) {
+  if (batch < 1 || h_kv < 1 || h_q < h_kv || d < 1) {
+    fail(SW_ERR_INVALID_ARG, "batch=%d h_q=%d h_kv=%d d=%d", batch, h_q, h_kv, d);
+    return -1;
+  }
+  ok();
+  const int64_t S = sw::decode_attn_splits(batch, h_kv);
+  return (int64_t)batch * h_q * S * (d + 2) * 4;
+}
+
+int sw_sparse_attn_decode(int dtype, const void* q, const void* Kc, const void* Vc, int batch,
+                          int h_q, int h_kv, int d, int T_max, int B, const int32_t* pos,
+                          const int32_t* idx, const int32_t* cnt, int kmax, float scale, void* O,
+                          void* workspace, int64_t workspace_bytes, void* stream) {
+  if (dtype != SW_F32 && dtype != SW_BF16) return fail(SW_ERR_INVALID_ARG, "dtype=%d", dtype);
+  CHECK(check_heads(h_q, h_kv));
+  const int G = h_q / h_kv;
+  if (G != 1 && G != 2 && G != 4 && G != 8)
+    return fail(SW_ERR_UNSUPPORTED, "decode attention needs h_q/h_kv in {1,2,4,8}, got %d", G);
+  if (d != 64 && d != 128) return fail(SW_ERR_UNSUPPORTED, "decode attention head dim d=%d (64 or 128)", d);
+  if (batch < 1 || batch > 65536) return fail(SW_ERR_INVALID_ARG, "batch=%d", batch);
+  if (T_max < 1) return fail(SW_ERR_INVALID_ARG, "T_max=%d", T_max);
+  if (B < 1 || B > 1024) return fail(SW_ERR_INVALID_ARG, "B=%d", B);
+  if (kmax < 1) return fail(SW_ERR_INVALID_ARG, "kmax=%d < 1", kmax);
+  CHECK(check_ptr(q, 16, "q"));
+  CHECK(check_ptr(Kc, 16, "Kc"));
+  CHECK(check_ptr(Vc, 16, "Vc"));
+  CHECK(check_ptr(O, 4, "O"));
+  CHECK(check_ptr(pos, 4, "pos"));
+  CHECK(check_ptr(idx, 4, "idx"));
+  CHECK(check_ptr(cnt, 4, "cnt"));
+  const int64_t need = sw_decode_attn_workspace_bytes(batch, h_q, h_kv, d);
+  CHECK(check_ptr(workspace, 256, "workspace"));
+  if (workspace_bytes < need)
+    return fail(SW_ERR_INVALID_ARG, "workspace_bytes=%lld < required %lld",
+                (long long)workspace_bytes, (long long)need);
+  if (!(scale > 0.0f)) scale = 1.0f / sqrtf((float)d);
+  hipError_t e = sw::launch_attn_decode(dtype, q, Kc, Vc, batch, h_q, h_kv, d, T_max, B, pos, idx,
+                                        cnt, kmax, scale, O, reinterpret_cast<float*>(workspace),
+                                        reinterpret_cast<hipStream_t>(stream));
+  return hip_status(e, "sw_sparse_attn_decode launch");
+}
+
 }  // extern "C"

@@ -8,6 +8,36 @@
 
 namespace sw {
 
+// Byte layout of one layer's decode state (every section 256-byte aligned):
+//   double A_scale[batch]        score scale c frozen at its prefill value
+//   int32  col0[batch]           first key block whose column decode fills
+//   int32  cnt[batch][2]         token counts of the open query / key block
+//   double bar[batch][2][d]      running means of the open query / key block
+//   double Qs[batch][b_max][r]   sketch of every query-block representative
+//   double Ks[batch][b_max][r]   sketch of every key-block representative
+//   float  A[batch][b_max][b_max] block-score cache
+struct DecodeLayout {
+  int64_t scale, col0, cnt, bar, qs, ks, a, total;
+};
+
+__host__ __device__ inline DecodeLayout decode_layout(int batch, int d, int r, int b_max) {
+  auto al = [](int64_t x) { return (x + 255) / 256 * 256; };
+  DecodeLayout L;
+  int64_t o = 0;
+  L.scale = o; o = al(o + 8LL * batch);
+  L.col0 = o;  o = al(o + 4LL * batch);
+  L.cnt = o;   o = al(o + 8LL * batch);
+  L.bar = o;   o = al(o + 16LL * batch * d);
+  L.qs = o;    o = al(o + 8LL * batch * b_max * r);
+  L.ks = o;    o = al(o + 8LL * batch * b_max * r);
+  L.a = o;     o = al(o + 4LL * batch * b_max * b_max);
+  L.total = o;
+  return L;
+}
+
+constexpr int kDecodeMaxSplits = 32;
+constexpr int kWalkRowChunk = 64;
+
 int64_t sketch_workspace_bytes(int h_q, int h_kv, int d, int64_t nb);
 
 hipError_t launch_sketch(int dtype, const void* Q, const void* K, int h_q, int h_kv, int d,
@@ -25,5 +55,34 @@ hipError_t launch_attn_prefill(int dtype, const void* Q, const void* K, const vo
                                int h_kv, int d, long long N, const SeqMeta& meta, int64_t nb,
                                const int32_t* idx, const int32_t* cnt, int kmax, float scale,
                                void* O, float* lse, hipStream_t st);
+
+hipError_t launch_decode_init(char* state, int batch, int d, int r, int b_max, int seq, int n, int B,
+                              const double* Qs, const double* Ks, const double* A,
+                              const double* A_scale, const double* Qbar, const double* Kbar,
+                              hipStream_t st);
+
+hipError_t launch_kv_append(int dtype, const void* k_new, const void* v_new, void* Kc, void* Vc,
+                            int batch, int h_kv, int d, int T_max, const int32_t* pos,
+                            hipStream_t st);
+
+hipError_t launch_decode_sketch(int dtype, const void* q_new, const void* k_new, int batch, int h_q,
+                                int h_kv, int d, int B, const int32_t* pos, const int8_t* signs,
+                                const int32_t* cols, int r, int b_max, char* state,
+                                hipStream_t st);
+
+hipError_t launch_decode_walk(const char* state, int batch, int d, int r, int b_max, int B,
+                              const int32_t* pos, int s_exp, const double* r_prev, double* r_out,
+                              double* partial, hipStream_t st);
+
+hipError_t launch_select_decode(const double* rows, int batch, int b_max, int B,
+                                const int32_t* pos, int k, int pct, uint32_t flags, int32_t* idx,
+                                int32_t* cnt, int kmax, hipStream_t st);
+
+int decode_attn_splits(int batch, int h_kv);
+
+hipError_t launch_attn_decode(int dtype, const void* q, const void* Kc, const void* Vc, int batch,
+                              int h_q, int h_kv, int d, int T_max, int B, const int32_t* pos,
+                              const int32_t* idx, const int32_t* cnt, int kmax, float scale,
+                              void* O, float* ws, hipStream_t st);
 
 }  // namespace sw
