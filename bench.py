@@ -108,6 +108,128 @@ def cpu_baseline(Qh, Kh, Vh, cu, B, signs, cols, s, pct, pairs, seed=0):
     }
 
 
+def run_decode(args, dev) -> dict:
+    """Decode workload: batch 16, 65536-token prompt per sequence, 32 layers,
+    256 single-token steps, every layer walked. Returns the decode block of
+    the JSON line."""
+    import torch
+    import synth
+    from paper_2602_07397_amd import binding as sw
+
+    w = synth.WORKLOADS["decode"]
+    L = args.decode_layers or w.layers
+    steps = args.decode_steps
+    batch, n0, B = w.batch, w.kv_len, w.B
+    T_max = n0 + steps
+    b_max = -(-T_max // B)
+    signs, cols = synth.srht_params(w.d, w.r, w.seed)
+    ts = torch.from_numpy(signs).to(dev)
+    tc = torch.from_numpy(cols).to(dev)
+    t0 = time.perf_counter()
+    Kc = [torch.empty((batch, w.h_kv, T_max, w.d), dtype=torch.bfloat16, device=dev) for _ in range(L)]
+    Vc = [torch.empty_like(Kc[0]) for _ in range(L)]
+    state = [sw.new_decode_state(batch, w.d, w.r, b_max, dev) for _ in range(L)]
+    for l in range(L):
+        for b in range(batch):
+            Q, K, V = synth.decode_prefix_inputs(w, l, b, device=dev)
+            sk = sw.sketch_scores(Q, K, [0, n0], B, ts, tc, want_means=True)
+            sw.decode_state_init(state[l], batch, w.d, w.r, b_max, b, n0, B, sk)
+            Kc[l][b, :, :n0] = K
+            Vc[l][b, :, :n0] = V
+            del Q, K, V, sk
+    toks = [[synth.decode_step_inputs(w, k, l, device=dev) for l in range(L)] for k in range(steps)]
+    torch.cuda.synchronize(dev)
+    print(f"[bench] decode setup {time.perf_counter() - t0:.1f} s", file=sys.stderr, flush=True)
+
+    kmax = sw.select_max_count_decode(b_max, density_pct=w.pct)
+    pos = torch.full((batch,), n0, dtype=torch.int32, device=dev)
+    rbuf = [torch.empty((batch, b_max), dtype=torch.float64, device=dev) for _ in range(2)]
+    idx = torch.empty((batch, kmax), dtype=torch.int32, device=dev)
+    cnt = torch.empty((batch,), dtype=torch.int32, device=dev)
+    obuf = torch.empty((batch, w.h_q, w.d), dtype=torch.bfloat16, device=dev)
+    wsw = torch.empty((sw.walk_decode_workspace_bytes(batch, b_max),), dtype=torch.uint8, device=dev)
+    wsa = torch.empty((sw.decode_attn_workspace_bytes(batch, w.h_q, w.h_kv, w.d),), dtype=torch.uint8,
+                      device=dev)
+    stream = torch.cuda.current_stream(dev)
+
+    def one_step(k, sel_log=None):
+        r = None
+        for l in range(L):
+            q, kk, v = toks[k][l]
+            sw.kv_append(kk, v, Kc[l], Vc[l], pos)
+            sw.sketch_scores_decode(q, kk, B, pos, ts, tc, b_max, state[l])
+            r = sw.walk_update_decode(state[l], batch, w.d, w.r, b_max, B, pos, w.s, r_prev=r,
+                                      r_out=rbuf[l & 1], workspace=wsw)
+            sw.select_topk_blocks_decode(r, B, pos, density_pct=w.pct, kmax=kmax, idx=idx, cnt=cnt)
+            if sel_log is not None:
+                sel_log.append((idx.clone(), cnt.clone()))
+            sw.sparse_attn_decode(q, Kc[l], Vc[l], B, pos, idx, cnt, kmax, O=obuf, workspace=wsa)
+        pos.add_(1)
+
+    # timed: all steps, whole path per step (append, sketch, walk, select, attention)
+    torch.cuda.synchronize(dev)
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for k in range(steps - 1):
+        one_step(k)
+    e1.record(stream)
+    torch.cuda.synchronize(dev)
+    total_ms = e0.elapsed_time(e1)
+    n_timed = steps - 1
+    wall_tok_s = batch * n_timed / (total_ms * 1e-3)
+
+    # last step with the selections kept, then the attention launches alone,
+    # back to back (the queue stays ahead of the host), for the roofline
+    sel_log = []
+    one_step(steps - 1, sel_log=sel_log)
+    pos.sub_(1)
+    torch.cuda.synchronize(dev)
+    reps = 3
+    a0 = torch.cuda.Event(enable_timing=True)
+    a1 = torch.cuda.Event(enable_timing=True)
+    a0.record(stream)
+    for _ in range(reps):
+        for l in range(L):
+            q = toks[steps - 1][l][0]
+            sw.sparse_attn_decode(q, Kc[l], Vc[l], B, pos, sel_log[l][0], sel_log[l][1], kmax, O=obuf,
+                                  workspace=wsa)
+    a1.record(stream)
+    torch.cuda.synchronize(dev)
+    attn_ms = a0.elapsed_time(a1) / (reps * L)
+    p = n0 + steps - 1
+    bc = p // B
+    kv_bytes = 0
+    for (it, ct) in sel_log:
+        ih, ch = it.cpu().numpy(), ct.cpu().numpy()
+        for b in range(batch):
+            toks_sel = 0
+            for j in ih[b, :ch[b]]:
+                toks_sel += B if j < bc else (p - bc * B + 1)
+            kv_bytes += toks_sel * w.h_kv * w.d * 2 * 2
+    qo_bytes = 2 * batch * w.h_q * w.d * 2 * L
+    attn_bytes = (kv_bytes + qo_bytes) / L
+    achieved = attn_bytes / (attn_ms * 1e-3) / 1e9
+    step_ms = total_ms / n_timed
+    sel_ms = step_ms / L - attn_ms
+    return {
+        "workload": "decode: batch 16, 65536-token KV cache, 32 q / 8 kv heads, head_dim 128, block 64, "
+                    "bf16, 32 layers, 256 steps, density 20%",
+        "tok_per_s": round(wall_tok_s, 1),
+        "ms_per_step": round(step_ms, 3),
+        "timed_steps": n_timed, "layers": L,
+        "attention_ms_per_layer": round(attn_ms, 4),
+        "rest_ms_per_layer": round(sel_ms, 4),
+        "overhead_pct": round(100.0 * max(sel_ms, 0.0) / (step_ms / L), 2),
+        "roofline": {
+            "kernel": "attn_decode_kernel<bf16,128,4> + attn_merge_kernel",
+            "bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+            "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None,
+            "avg_launch_ms": round(attn_ms, 4), "bytes_per_launch": attn_bytes,
+        },
+    }
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -116,6 +238,9 @@ def main() -> int:
     ap.add_argument("--layers", type=int, default=None, help="override layer count (debug only)")
     ap.add_argument("--cpu-pairs", type=int, default=192)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-decode", action="store_true")
+    ap.add_argument("--decode-steps", type=int, default=256)
+    ap.add_argument("--decode-layers", type=int, default=None, help="override (debug only)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU; --gpus must be 1"}))
@@ -255,6 +380,13 @@ def main() -> int:
             "flop_per_launch": flops_alg / L,
         },
     }
+    if not args.no_decode:
+        del bufs, ws, Rbuf, idx, cnt, Obuf
+        layers_keep = layers[0] if not args.no_cpu_baseline else None
+        layers = None
+        torch.cuda.empty_cache()
+        out["decode"] = run_decode(args, dev)
+        layers = [layers_keep]
     if not args.no_cpu_baseline:
         Q, K, V = layers[0]
         Qh, Kh, Vh = Q.cpu(), K.cpu(), V.cpu()
