@@ -147,32 +147,55 @@ def run_decode(args, dev) -> dict:
     idx = torch.empty((batch, kmax), dtype=torch.int32, device=dev)
     cnt = torch.empty((batch,), dtype=torch.int32, device=dev)
     obuf = torch.empty((batch, w.h_q, w.d), dtype=torch.bfloat16, device=dev)
-    wsw = torch.empty((sw.walk_decode_workspace_bytes(batch, b_max),), dtype=torch.uint8, device=dev)
     wsa = torch.empty((sw.decode_attn_workspace_bytes(batch, w.h_q, w.h_kv, w.d),), dtype=torch.uint8,
                       device=dev)
     stream = torch.cuda.current_stream(dev)
 
-    def one_step(k, sel_log=None):
+    # inputs for every step, and the fixed per-step buffers a captured graph reads
+    tq = torch.stack([torch.stack([toks[k][l][0] for l in range(L)]) for k in range(steps)])
+    tk = torch.stack([torch.stack([toks[k][l][1] for l in range(L)]) for k in range(steps)])
+    tv = torch.stack([torch.stack([toks[k][l][2] for l in range(L)]) for k in range(steps)])
+    del toks
+    bq, bk, bv = torch.empty_like(tq[0]), torch.empty_like(tk[0]), torch.empty_like(tv[0])
+
+    def body(sel_log=None):
         r = None
         for l in range(L):
-            q, kk, v = toks[k][l]
-            sw.kv_append(kk, v, Kc[l], Vc[l], pos)
-            sw.sketch_scores_decode(q, kk, B, pos, ts, tc, b_max, state[l])
+            sw.kv_append(bk[l], bv[l], Kc[l], Vc[l], pos)
+            sw.sketch_scores_decode(bq[l], bk[l], B, pos, ts, tc, b_max, state[l])
             r = sw.walk_update_decode(state[l], batch, w.d, w.r, b_max, B, pos, w.s, r_prev=r,
-                                      r_out=rbuf[l & 1], workspace=wsw)
+                                      r_out=rbuf[l & 1])
             sw.select_topk_blocks_decode(r, B, pos, density_pct=w.pct, kmax=kmax, idx=idx, cnt=cnt)
             if sel_log is not None:
                 sel_log.append((idx.clone(), cnt.clone()))
-            sw.sparse_attn_decode(q, Kc[l], Vc[l], B, pos, idx, cnt, kmax, O=obuf, workspace=wsa)
+            sw.sparse_attn_decode(bq[l], Kc[l], Vc[l], B, pos, idx, cnt, kmax, O=obuf, workspace=wsa)
         pos.add_(1)
 
-    # timed: all steps, whole path per step (append, sketch, walk, select, attention)
+    def load_inputs(k):
+        bq.copy_(tq[k])
+        bk.copy_(tk[k])
+        bv.copy_(tv[k])
+
+    graph = None
+    if not args.decode_eager:
+        torch.cuda.synchronize(dev)
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            body()
+        torch.cuda.synchronize(dev)
+
+    # timed: steps 0..steps-2, each the whole path for all layers (input copy,
+    # KV append, sketch, walk, select, attention)
     torch.cuda.synchronize(dev)
     e0 = torch.cuda.Event(enable_timing=True)
     e1 = torch.cuda.Event(enable_timing=True)
     e0.record(stream)
     for k in range(steps - 1):
-        one_step(k)
+        load_inputs(k)
+        if graph is not None:
+            graph.replay()
+        else:
+            body()
     e1.record(stream)
     torch.cuda.synchronize(dev)
     total_ms = e0.elapsed_time(e1)
@@ -182,7 +205,8 @@ def run_decode(args, dev) -> dict:
     # last step with the selections kept, then the attention launches alone,
     # back to back (the queue stays ahead of the host), for the roofline
     sel_log = []
-    one_step(steps - 1, sel_log=sel_log)
+    load_inputs(steps - 1)
+    body(sel_log=sel_log)
     pos.sub_(1)
     torch.cuda.synchronize(dev)
     reps = 3
@@ -191,8 +215,7 @@ def run_decode(args, dev) -> dict:
     a0.record(stream)
     for _ in range(reps):
         for l in range(L):
-            q = toks[steps - 1][l][0]
-            sw.sparse_attn_decode(q, Kc[l], Vc[l], B, pos, sel_log[l][0], sel_log[l][1], kmax, O=obuf,
+            sw.sparse_attn_decode(bq[l], Kc[l], Vc[l], B, pos, sel_log[l][0], sel_log[l][1], kmax, O=obuf,
                                   workspace=wsa)
     a1.record(stream)
     torch.cuda.synchronize(dev)
@@ -218,6 +241,7 @@ def run_decode(args, dev) -> dict:
         "tok_per_s": round(wall_tok_s, 1),
         "ms_per_step": round(step_ms, 3),
         "timed_steps": n_timed, "layers": L,
+        "launch": "eager" if graph is None else "hip graph of the 32-layer step",
         "attention_ms_per_layer": round(attn_ms, 4),
         "rest_ms_per_layer": round(sel_ms, 4),
         "overhead_pct": round(100.0 * max(sel_ms, 0.0) / (step_ms / L), 2),
@@ -230,23 +254,9 @@ def run_decode(args, dev) -> dict:
     }
 
 
-def main() -> int:
-    ap = argparse.ArgumentParser()
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=5)
-    ap.add_argument("--warmup", type=int, default=1)
-    ap.add_argument("--layers", type=int, default=None, help="override layer count (debug only)")
-    ap.add_argument("--cpu-pairs", type=int, default=192)
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-decode", action="store_true")
-    ap.add_argument("--decode-steps", type=int, default=256)
-    ap.add_argument("--decode-layers", type=int, default=None, help="override (debug only)")
-    args = ap.parse_args()
-    if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU; --gpus must be 1"}))
-        print("bench.py: only --gpus 1 is supported (one GPU per run)", file=sys.stderr)
-        return 2
-
+def run_prefill(args, dev):
+    """Prefill workload (32 layers of the Llama-3-8B shape). Returns the
+    JSON fields and a host copy of layer 0's inputs for the CPU baseline."""
     import torch
     import synth
     from paper_2602_07397_amd import binding as sw
@@ -380,19 +390,47 @@ def main() -> int:
             "flop_per_launch": flops_alg / L,
         },
     }
-    if not args.no_decode:
-        del bufs, ws, Rbuf, idx, cnt, Obuf
-        layers_keep = layers[0] if not args.no_cpu_baseline else None
-        layers = None
+    Q, K, V = layers[0]
+    cpu_layer = (Q.cpu(), K.cpu(), V.cpu())
+    return out, cpu_layer
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--layers", type=int, default=None, help="override layer count (debug only)")
+    ap.add_argument("--cpu-pairs", type=int, default=192)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-decode", action="store_true")
+    ap.add_argument("--decode-steps", type=int, default=256)
+    ap.add_argument("--decode-layers", type=int, default=None, help="override (debug only)")
+    ap.add_argument("--decode-eager", action="store_true", help="launch the decode step eagerly")
+    ap.add_argument("--only", choices=("prefill", "decode"), default=None,
+                    help="run one workload only (profiling); the JSON line then lacks the other")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU; --gpus must be 1"}))
+        print("bench.py: only --gpus 1 is supported (one GPU per run)", file=sys.stderr)
+        return 2
+
+    import torch
+    dev = torch.device("cuda:0")
+    out = {}
+    cpu_layer = None
+    if args.only != "decode":
+        out, cpu_layer = run_prefill(args, dev)
         torch.cuda.empty_cache()
+    if args.only != "prefill" and not args.no_decode:
         out["decode"] = run_decode(args, dev)
-        layers = [layers_keep]
-    if not args.no_cpu_baseline:
-        Q, K, V = layers[0]
-        Qh, Kh, Vh = Q.cpu(), K.cpu(), V.cpu()
+    if cpu_layer is not None and not args.no_cpu_baseline:
+        import synth
+        w = synth.WORKLOADS["llama8b"]
+        signs, cols = synth.srht_params(w.d, w.r, w.seed)
         print("[bench] timing the oracle on the host", file=sys.stderr, flush=True)
-        out["cpu_baseline"] = cpu_baseline(Qh, Kh, Vh, cu, B, signs, cols, w.s, w.pct,
-                                           args.cpu_pairs)
+        out["cpu_baseline"] = cpu_baseline(*cpu_layer, synth.cu_seqlens(w.seqlens), w.B, signs, cols,
+                                           w.s, w.pct, args.cpu_pairs)
     print(json.dumps(out), flush=True)
     return 0
 

@@ -182,9 +182,11 @@ int sw_sparse_attn_prefill(int dtype, const void* Q, const void* K, const void* 
  *                                 (= prompt length / B)
  *   int32  cnt[batch][2]          token counts of the open query / key block
  *   double bar[batch][2][d]       running means of the open query / key block
+ *   double qt[batch][r]           sketch of the latest token's query
  *   double Qs[batch][b_max][r]    sketch of every query-block representative
  *   double Ks[batch][b_max][r]    sketch of every key-block representative
- *   float  A[batch][b_max][b_max] block-score cache (fp32)
+ *   float  A[batch][b_max][lda]   block-score cache (fp32), lda = b_max rounded
+ *                                 up to a multiple of 4
  * Checkpointing a decode is a byte copy of this buffer (plus the caches).
  * pos [batch] int32 (device): 0-based position of the new token of each
  * sequence; b_cur = pos / B is the open block. Sequences whose pos is
@@ -227,20 +229,17 @@ int sw_sketch_scores_decode(int dtype, const void* q_new, const void* k_new, int
                             int h_kv, int d, int B, const int32_t* pos, const int8_t* signs,
                             const int32_t* cols, int r, int b_max, void* state, void* stream);
 
-/* Host-only: workspace bytes of sw_walk_update_decode (-1 on bad input). */
-int64_t sw_walk_decode_workspace_bytes(int batch, int b_max);
-
 /*
  * sw_walk_update_decode - Alg. 2 step 5 on the current query row:
  *   r_out = W[b_cur, :] if r_prev is NULL (first walked layer), else
  *   r_prev W, with W = (A / c)^s element-wise over the layer's score cache;
  *   then divided by its largest magnitude. r_prev, r_out [batch][b_max]
- *   float64 (entries past b_cur are written as 0); the workspace is needed
- *   when r_prev is given. Sums run in fp64 in a fixed order.
+ *   float64 (entries past b_cur are written as 0; r_out must not alias
+ *   r_prev). Sums run in fp64 in a fixed order.
  */
 int sw_walk_update_decode(const void* state, int batch, int d, int r, int b_max, int B,
                           const int32_t* pos, int s, const double* r_prev, double* r_out,
-                          void* workspace, int64_t workspace_bytes, void* stream);
+                          void* stream);
 
 /* Host-only: the largest decode budget over rows of up to b_max blocks. */
 int sw_select_max_count_decode(int b_max, int k, int density_pct, uint32_t flags, int32_t* kmax);

@@ -53,9 +53,8 @@ _SIGNATURES = {
     "sw_kv_append": (_c_int, [_c_int, _vp, _vp, _vp, _vp, _c_int, _c_int, _c_int, _c_int, _vp, _vp]),
     "sw_sketch_scores_decode": (_c_int, [_c_int, _vp, _vp, _c_int, _c_int, _c_int, _c_int, _c_int, _vp,
                                          _vp, _vp, _c_int, _c_int, _vp, _vp]),
-    "sw_walk_decode_workspace_bytes": (_c_i64, [_c_int, _c_int]),
     "sw_walk_update_decode": (_c_int, [_vp, _c_int, _c_int, _c_int, _c_int, _c_int, _vp, _c_int, _vp,
-                                       _vp, _vp, _c_i64, _vp]),
+                                       _vp, _vp]),
     "sw_select_max_count_decode": (_c_int, [_c_int, _c_int, _c_int, ctypes.c_uint32, _i32p]),
     "sw_select_topk_blocks_decode": (_c_int, [_vp, _c_int, _c_int, _c_int, _vp, _c_int, _c_int,
                                               ctypes.c_uint32, _vp, _vp, _c_int, _vp]),
@@ -304,28 +303,16 @@ def sketch_scores_decode(q_new: torch.Tensor, k_new: torch.Tensor, B: int, pos: 
     _check(rc, "sw_sketch_scores_decode")
 
 
-def walk_decode_workspace_bytes(batch: int, b_max: int) -> int:
-    v = load().sw_walk_decode_workspace_bytes(batch, b_max)
-    if v < 0:
-        _check(1, "sw_walk_decode_workspace_bytes")
-    return int(v)
-
-
 def walk_update_decode(state: torch.Tensor, batch: int, d: int, r: int, b_max: int, B: int,
                        pos: torch.Tensor, s: int, r_prev: Optional[torch.Tensor] = None,
-                       r_out: Optional[torch.Tensor] = None,
-                       workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
+                       r_out: Optional[torch.Tensor] = None) -> torch.Tensor:
     dev = state.device
     if r_out is None:
         r_out = torch.empty((batch, b_max), dtype=torch.float64, device=dev)
-    wsb = walk_decode_workspace_bytes(batch, b_max)
-    if workspace is None or workspace.numel() < wsb:
-        workspace = torch.empty((wsb,), dtype=torch.uint8, device=dev)
     rc = load().sw_walk_update_decode(_dev(state, "state", torch.uint8), batch, d, r, b_max, B,
                                       _dev(pos, "pos", torch.int32), s,
                                       _opt(r_prev, "r_prev", torch.float64),
-                                      _dev(r_out, "r_out", torch.float64), _dev(workspace, "workspace"),
-                                      workspace.numel(), _stream(dev))
+                                      _dev(r_out, "r_out", torch.float64), _stream(dev))
     _check(rc, "sw_walk_update_decode")
     return r_out
 

@@ -351,19 +351,9 @@ int sw_sketch_scores_decode(int dtype, const void* q_new, const void* k_new, int
   return hip_status(e, "sw_sketch_scores_decode launch");
 }
 
-int64_t sw_walk_decode_workspace_bytes(int batch, int b_max) {
-  if (batch < 1 || b_max < 1 || b_max > SW_MAX_BLOCKS) {
-    fail(SW_ERR_INVALID_ARG, "batch=%d b_max=%d", batch, b_max);
-    return -1;
-  }
-  ok();
-  const int64_t nch = (b_max + sw::kWalkRowChunk - 1) / sw::kWalkRowChunk;
-  return (int64_t)batch * nch * b_max * 8;
-}
-
 int sw_walk_update_decode(const void* state, int batch, int d, int r, int b_max, int B,
                           const int32_t* pos, int s, const double* r_prev, double* r_out,
-                          void* workspace, int64_t workspace_bytes, void* stream) {
+                          void* stream) {
   if (s < 1 || s > 64) return fail(SW_ERR_INVALID_ARG, "s=%d outside [1, 64]", s);
   CHECK(check_decode_shape(batch, d, r, b_max, B));
   CHECK(check_ptr(state, 256, "state"));
@@ -371,16 +361,8 @@ int sw_walk_update_decode(const void* state, int batch, int d, int r, int b_max,
   CHECK(check_ptr(r_out, 8, "r_out"));
   if (r_prev && !aligned(r_prev, 8)) return fail(SW_ERR_INVALID_ARG, "r_prev misaligned");
   if (r_prev == r_out) return fail(SW_ERR_INVALID_ARG, "r_out aliases r_prev");
-  if (r_prev) {
-    const int64_t need = sw_walk_decode_workspace_bytes(batch, b_max);
-    CHECK(check_ptr(workspace, 256, "workspace"));
-    if (workspace_bytes < need)
-      return fail(SW_ERR_INVALID_ARG, "workspace_bytes=%lld < required %lld",
-                  (long long)workspace_bytes, (long long)need);
-  }
   hipError_t e = sw::launch_decode_walk(reinterpret_cast<const char*>(state), batch, d, r, b_max, B,
-                                        pos, s, r_prev, r_out, reinterpret_cast<double*>(workspace),
-                                        reinterpret_cast<hipStream_t>(stream));
+                                        pos, s, r_prev, r_out, reinterpret_cast<hipStream_t>(stream));
   return hip_status(e, "sw_walk_update_decode launch");
 }
 

@@ -2,17 +2,19 @@
 //
 //  decode_init_kernel     state of one sequence from its prompt's prefill sketch
 //  kv_append_kernel       step 1: K_t, V_t into the caches at pos[b]
-//  decode_sketch_kernel   steps 2-4: running means of the open query/key
-//                         block, SRHT of the token query and of both open
-//                         representatives (in-LDS FWHT), new score row
-//                         (token query vs every key block) and new last column
-//                         (every query block vs the open key block)
-//  walk_row_partial/finish step 5 on the query row only: r = W[b_q, :] at the
-//                         first walked layer, else r_prev W, with W = (A/c)^s
-//                         taken while streaming the fp32 score cache; partial
-//                         sums over 64-row chunks are reduced in a fixed order
-//                         (deterministic), then the row is divided by its
-//                         largest magnitude
+//  decode_reps_kernel     steps 2-3 (one workgroup per sequence): running means
+//                         of the open query/key block, SRHT (in-LDS FWHT) of the
+//                         token query and of both open representatives
+//  decode_scores_kernel   step 4 over (sequence, 64-row chunk) workgroups, 16
+//                         lanes per 64-wide sketch row: (i) new score row (token
+//                         query vs every earlier key block), (ii) new last
+//                         column (every query block vs the open key block)
+//  walk_row_strip_kernel  step 5 on the query row only: r = W[b_q, :] at the
+//                         first walked layer, else r_prev W with W = (A/c)^s
+//                         taken while streaming the fp32 score cache; one
+//                         workgroup per (sequence, 32-column strip), 32 row
+//                         groups reduced in LDS in a fixed order
+//  walk_row_norm_kernel   divides the row by its largest magnitude
 //  attn_decode_kernel     step 7, split-K: each workgroup streams an equal share
 //                         of the selected tokens of one (sequence, KV head) for
 //                         all G query heads of the group with 16-byte loads and
@@ -24,6 +26,7 @@
 namespace sw {
 
 constexpr float kLog2eD = 1.4426950408889634f;
+constexpr int kDecodeSelCache = 512;   // selected-block entries cached per workgroup
 
 __device__ __forceinline__ double pow_int_d(double x, int s) {
   double r = 1.0, b = x;
@@ -50,8 +53,8 @@ __global__ __launch_bounds__(256) void decode_init_kernel(char* __restrict__ sta
   const DecodeLayout L = decode_layout(batch, d, r, b_max);
   const int m = blockIdx.x;              // row of the score cache
   const int b = (n + B - 1) / B;
-  float* Arow = reinterpret_cast<float*>(state + L.a) + ((long long)seq * b_max + m) * b_max;
-  for (int j = threadIdx.x; j < b_max; j += 256)
+  float* Arow = reinterpret_cast<float*>(state + L.a) + ((long long)seq * b_max + m) * L.lda;
+  for (int j = threadIdx.x; j < L.lda; j += 256)
     Arow[j] = (m < b && j < b) ? (float)A[(long long)m * b + j] : 0.0f;
   if (m < b) {
     double* qs = reinterpret_cast<double*>(state + L.qs) + ((long long)seq * b_max + m) * r;
@@ -103,25 +106,25 @@ __global__ __launch_bounds__(64) void kv_append_kernel(const T* __restrict__ k_n
 // ---------------------------------------------------------------------------
 
 template <typename T>
-__device__ __forceinline__ double load_f64(const T* p, long long i) {
+__device__ __forceinline__ float load_f32(const T* p, long long i) {
   if constexpr (sizeof(T) == 2) {
-    return (double)bf16_to_f32(reinterpret_cast<const uint16_t*>(p)[i]);
+    return bf16_to_f32(reinterpret_cast<const uint16_t*>(p)[i]);
   } else {
-    return (double)p[i];
+    return p[i];
   }
 }
 
 template <typename T>
-__global__ __launch_bounds__(256) void decode_sketch_kernel(const T* __restrict__ q_new,
-                                                            const T* __restrict__ k_new, int h_q,
-                                                            int h_kv, int d, int B,
-                                                            const int32_t* __restrict__ pos,
-                                                            const int8_t* __restrict__ signs,
-                                                            const int32_t* __restrict__ cols, int r,
-                                                            int batch, int b_max,
-                                                            char* __restrict__ state) {
+__global__ __launch_bounds__(256) void decode_reps_kernel(const T* __restrict__ q_new,
+                                                          const T* __restrict__ k_new, int h_q,
+                                                          int h_kv, int d, int B,
+                                                          const int32_t* __restrict__ pos,
+                                                          const int8_t* __restrict__ signs,
+                                                          const int32_t* __restrict__ cols, int r,
+                                                          int batch, int b_max,
+                                                          char* __restrict__ state) {
   __shared__ double xq[256], xk[256], xb[256];
-  __shared__ double qt[256], kn[256], qn[256];
+  __shared__ double pq[256], pk[256];
   const DecodeLayout L = decode_layout(batch, d, r, b_max);
   const int bi = blockIdx.x;
   const int t = threadIdx.x;
@@ -132,13 +135,24 @@ __global__ __launch_bounds__(256) void decode_sketch_kernel(const T* __restrict_
   int32_t* cnt = reinterpret_cast<int32_t*>(state + L.cnt) + bi * 2;
   double* Qs = reinterpret_cast<double*>(state + L.qs) + (long long)bi * b_max * r;
   double* Ks = reinterpret_cast<double*>(state + L.ks) + (long long)bi * b_max * r;
-  float* A = reinterpret_cast<float*>(state + L.a) + (long long)bi * b_max * b_max;
+  double* qt = reinterpret_cast<double*>(state + L.qt) + (long long)bi * r;
+  // head sums: thread (part, dim) adds the heads u = part, part + P, ...
+  const int P = 256 / d;
+  const int dim = t % d, part = t / d;
+  double sq = 0.0, sk = 0.0;
+  for (int u = part; u < h_q; u += P) sq += (double)load_f32(q_new, ((long long)bi * h_q + u) * d + dim);
+  for (int g = part; g < h_kv; g += P) sk += (double)load_f32(k_new, ((long long)bi * h_kv + g) * d + dim);
+  pq[t] = sq;
+  pk[t] = sk;
   const bool fresh = (p % B) == 0;
   const int qc = cnt[0], kc = cnt[1];
+  __syncthreads();
   double qa = 0.0, ka = 0.0, qbn = 0.0, kbn = 0.0;
   if (t < d) {
-    for (int u = 0; u < h_q; ++u) qa += load_f64(q_new, ((long long)bi * h_q + u) * d + t);
-    for (int g = 0; g < h_kv; ++g) ka += load_f64(k_new, ((long long)bi * h_kv + g) * d + t);
+    for (int x = 0; x < P; ++x) {
+      qa += pq[x * d + t];
+      ka += pk[x * d + t];
+    }
     qa /= (double)h_q;
     ka /= (double)h_kv;
     qbn = fresh ? qa : ((double)qc * bar[t] + qa) / (double)(qc + 1);
@@ -172,37 +186,53 @@ __global__ __launch_bounds__(256) void decode_sketch_kernel(const T* __restrict_
   if (t < r) {
     const int c = cols[t] & (d - 1);
     qt[t] = xq[c] * rs;
-    qn[t] = xb[c] * rs;
-    kn[t] = xk[c] * rs;
-    Qs[(long long)bc * r + t] = qn[t];
-    Ks[(long long)bc * r + t] = kn[t];
+    Qs[(long long)bc * r + t] = xb[c] * rs;
+    Ks[(long long)bc * r + t] = xk[c] * rs;
   }
-  __syncthreads();
-  // groups of 8 lanes per dot product
-  const int grp = t >> 3, sub = t & 7;
-  // (i) new query row: token query vs key blocks j < bc (j = bc comes from (ii))
-  for (int j0 = 0; j0 < bc; j0 += 32) {
-    const int j = j0 + grp;
-    double acc = 0.0;
-    if (j < bc)
-      for (int k = sub; k < r; k += 8) acc += qt[k] * Ks[(long long)j * r + k];
-    acc += __shfl_xor(acc, 4);
-    acc += __shfl_xor(acc, 2);
-    acc += __shfl_xor(acc, 1);
-    if (j < bc && sub == 0) A[(long long)bc * b_max + j] = (float)(acc * rs);
-  }
-  // (ii) last column: query blocks m <= bc vs the open key block
-  for (int m0 = 0; m0 <= bc; m0 += 32) {
-    const int m = m0 + grp;
-    double acc = 0.0;
-    if (m <= bc) {
-      const double* qrow = (m == bc) ? qn : Qs + (long long)m * r;
-      for (int k = sub; k < r; k += 8) acc += qrow[k] * kn[k];
+}
+
+constexpr int kScoreChunk = 64;
+
+// Rows [64c, 64c+64): row entries A[bc][j] (j < bc) and column entries
+// A[m][bc] (m <= bc). 16 lanes per 64-wide row (lane sub takes elements
+// sub, sub+16, ...), 16 rows per pass of the 256 threads.
+__global__ __launch_bounds__(256) void decode_scores_kernel(const int32_t* __restrict__ pos, int r,
+                                                            int B, int batch, int d, int b_max,
+                                                            char* __restrict__ state) {
+  const DecodeLayout L = decode_layout(batch, d, r, b_max);
+  const int bi = blockIdx.x;
+  const int c = blockIdx.y;
+  const int p = pos[bi];
+  const int bc = p / B;
+  if (p < 0 || bc >= b_max) return;
+  const int r0 = c * kScoreChunk;
+  if (r0 > bc) return;
+  const double* Qs = reinterpret_cast<const double*>(state + L.qs) + (long long)bi * b_max * r;
+  const double* Ks = reinterpret_cast<const double*>(state + L.ks) + (long long)bi * b_max * r;
+  const double* qt = reinterpret_cast<const double*>(state + L.qt) + (long long)bi * r;
+  float* A = reinterpret_cast<float*>(state + L.a) + (long long)bi * b_max * L.lda;
+  const double rs = 1.0 / sqrt((double)r);
+  const int t = threadIdx.x;
+  const int sub = t & 15, rr = t >> 4;
+  for (int pass = 0; pass < kScoreChunk / 16; ++pass) {
+    const int j = r0 + pass * 16 + rr;
+    double accr = 0.0, accc = 0.0;
+    if (j <= bc) {
+      for (int k = sub; k < r; k += 16) {
+        const double kb = Ks[(long long)bc * r + k];
+        accc += Qs[(long long)j * r + k] * kb;
+        if (j < bc) accr += qt[k] * Ks[(long long)j * r + k];
+      }
     }
-    acc += __shfl_xor(acc, 4);
-    acc += __shfl_xor(acc, 2);
-    acc += __shfl_xor(acc, 1);
-    if (m <= bc && sub == 0) A[(long long)m * b_max + bc] = (float)(acc * rs);
+#pragma unroll
+    for (int off = 8; off > 0; off >>= 1) {
+      accr += __shfl_xor(accr, off);
+      accc += __shfl_xor(accc, off);
+    }
+    if (sub == 0 && j <= bc) {
+      if (j < bc) A[(long long)bc * L.lda + j] = (float)(accr * rs);
+      A[(long long)j * L.lda + bc] = (float)(accc * rs);
+    }
   }
 }
 
@@ -210,83 +240,102 @@ __global__ __launch_bounds__(256) void decode_sketch_kernel(const T* __restrict_
 // walk row
 // ---------------------------------------------------------------------------
 
-__global__ __launch_bounds__(256) void walk_row_partial_kernel(const char* __restrict__ state,
-                                                               int batch, int d, int r, int b_max,
-                                                               int B, const int32_t* __restrict__ pos,
-                                                               int s_exp,
-                                                               const double* __restrict__ r_prev,
-                                                               double* __restrict__ partial) {
+constexpr int kStrip = 32;       // columns per workgroup (8 lanes x 4)
+constexpr int kRowGroups = 32;   // row groups per workgroup
+
+__global__ __launch_bounds__(256) void walk_row_strip_kernel(const char* __restrict__ state,
+                                                             int batch, int d, int r, int b_max,
+                                                             int B, const int32_t* __restrict__ pos,
+                                                             int s_exp,
+                                                             const double* __restrict__ r_prev,
+                                                             double* __restrict__ r_out) {
+  __shared__ double red[kRowGroups][kStrip];
   const DecodeLayout L = decode_layout(batch, d, r, b_max);
   const int bi = blockIdx.x;
-  const int ch = blockIdx.y;
+  const int j0 = blockIdx.y * kStrip;
   const int p = pos[bi];
   const int bc = p / B;
   if (p < 0 || bc >= b_max) return;
-  const int m0 = ch * kWalkRowChunk;
-  if (m0 > bc) return;
-  const int m1 = min(m0 + kWalkRowChunk, bc + 1);
+  if (j0 > bc) return;
   const double c0 = reinterpret_cast<const double*>(state + L.scale)[bi];
   const double inv_c = 1.0 / (c0 > 0.0 ? c0 : 1.0);
   const int col0 = reinterpret_cast<const int32_t*>(state + L.col0)[bi];
-  const float* A = reinterpret_cast<const float*>(state + L.a) + (long long)bi * b_max * b_max;
-  const double* rp = r_prev + (long long)bi * b_max;
-  const int nch = (b_max + kWalkRowChunk - 1) / kWalkRowChunk;
-  double* out = partial + ((long long)bi * nch + ch) * b_max;
-  __shared__ double rv[kWalkRowChunk];
-  for (int m = m0 + threadIdx.x; m < m1; m += 256) rv[m - m0] = rp[m];
-  __syncthreads();
-  for (int j = threadIdx.x; j <= bc; j += 256) {
-    double acc = 0.0;
-    // W[m][j] can be non-zero for j <= m (causal) or j >= col0 (columns
-    // filled by decode for every earlier query block)
-    if (j < m1 || j >= col0) {
-      const int mlo = (j >= col0) ? m0 : max(m0, j);
-      for (int m = mlo; m < m1; ++m)
-        acc += rv[m - m0] * pow_int_d((double)A[(long long)m * b_max + j] * inv_c, s_exp);
+  const float* A = reinterpret_cast<const float*>(state + L.a) + (long long)bi * b_max * L.lda;
+  const int t = threadIdx.x;
+  const int cq = t & 7, rg = t >> 3;
+  const int j = j0 + cq * 4;                       // first of this thread's 4 columns
+  const bool jok = j < L.lda;                      // lda % 4 == 0: j..j+3 inside the row
+  double acc[4] = {0.0, 0.0, 0.0, 0.0};
+  if (!jok) {
+    // columns past the padded row: nothing to accumulate
+  } else if (r_prev == nullptr) {
+    // first walked layer: the query row of W itself
+    if (rg == 0) {
+      const float4 a = *reinterpret_cast<const float4*>(A + (long long)bc * L.lda + j);
+      const float av[4] = {a.x, a.y, a.z, a.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) acc[e] = pow_int_d((double)av[e] * inv_c, s_exp);
     }
-    out[j] = acc;
+  } else {
+    const double* rp = r_prev + (long long)bi * b_max;
+    // rows that can be non-zero in these columns: m >= column (causal) or any
+    // row for the columns decode filled (>= col0)
+    const int mstart = (j0 + kStrip - 1 >= col0) ? 0 : j0;
+    int m = mstart + rg;
+    for (; m + 7 * kRowGroups <= bc; m += 8 * kRowGroups) {
+      float4 a[8];
+      double w[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        a[u] = *reinterpret_cast<const float4*>(A + (long long)(m + u * kRowGroups) * L.lda + j);
+        w[u] = rp[m + u * kRowGroups];
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int mm = m + u * kRowGroups;
+        const float av[4] = {a[u].x, a[u].y, a[u].z, a[u].w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (j + e <= mm || j + e >= col0) acc[e] += w[u] * pow_int_d((double)av[e] * inv_c, s_exp);
+      }
+    }
+    for (; m <= bc; m += kRowGroups) {
+      const float4 a = *reinterpret_cast<const float4*>(A + (long long)m * L.lda + j);
+      const double wv = rp[m];
+      const float av[4] = {a.x, a.y, a.z, a.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (j + e <= m || j + e >= col0) acc[e] += wv * pow_int_d((double)av[e] * inv_c, s_exp);
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < 4; ++e) red[rg][cq * 4 + e] = acc[e];
+  __syncthreads();
+  if (t < kStrip) {
+    double v = 0.0;
+    for (int g = 0; g < kRowGroups; ++g) v += red[g][t];
+    const int jj = j0 + t;
+    if (jj < b_max) r_out[(long long)bi * b_max + jj] = (jj <= bc) ? v : 0.0;
   }
 }
 
-__global__ __launch_bounds__(256) void walk_row_finish_kernel(const char* __restrict__ state,
-                                                              int batch, int d, int r, int b_max,
-                                                              int B, const int32_t* __restrict__ pos,
-                                                              int s_exp, int first,
-                                                              const double* __restrict__ partial,
-                                                              double* __restrict__ r_out) {
+__global__ __launch_bounds__(256) void walk_row_norm_kernel(int b_max, int B,
+                                                            const int32_t* __restrict__ pos,
+                                                            double* __restrict__ r_out) {
   __shared__ double tmp[4];
-  const DecodeLayout L = decode_layout(batch, d, r, b_max);
   const int bi = blockIdx.x;
   const int p = pos[bi];
   const int bc = p / B;
   if (p < 0 || bc >= b_max) return;
-  const double c0 = reinterpret_cast<const double*>(state + L.scale)[bi];
-  const double inv_c = 1.0 / (c0 > 0.0 ? c0 : 1.0);
-  const float* Arow = reinterpret_cast<const float*>(state + L.a) + ((long long)bi * b_max + bc) * b_max;
-  const int nch = (b_max + kWalkRowChunk - 1) / kWalkRowChunk;
-  const int used = bc / kWalkRowChunk + 1;
   double* out = r_out + (long long)bi * b_max;
   double mx = 0.0;
-  for (int j = threadIdx.x; j < b_max; j += 256) {
-    double v = 0.0;
-    if (j <= bc) {
-      if (first) {
-        v = pow_int_d((double)Arow[j] * inv_c, s_exp);
-      } else {
-        for (int c = 0; c < used; ++c) v += partial[((long long)bi * nch + c) * b_max + j];
-      }
-    }
-    out[j] = v;
-    mx = fmax(mx, fabs(v));
-  }
+  for (int j = threadIdx.x; j <= bc; j += 256) mx = fmax(mx, fabs(out[j]));
   for (int off = 32; off > 0; off >>= 1) mx = fmax(mx, __shfl_xor(mx, off));
   if ((threadIdx.x & 63) == 0) tmp[threadIdx.x >> 6] = mx;
   __syncthreads();
   mx = fmax(fmax(tmp[0], tmp[1]), fmax(tmp[2], tmp[3]));
-  if (mx > 0.0) {
-    const double inv = 1.0 / mx;
-    for (int j = threadIdx.x; j <= bc; j += 256) out[j] = out[j] * inv;
-  }
+  const double inv = mx > 0.0 ? 1.0 / mx : 1.0;
+  for (int j = threadIdx.x; j < b_max; j += 256) out[j] = (j <= bc) ? out[j] * inv : 0.0;
 }
 
 // ---------------------------------------------------------------------------
@@ -351,54 +400,102 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(const T* __restrict__ 
   const T* Kb = Kc + (long long)bg * T_max * D + sub * EPL;
   const T* Vb = Vc + (long long)bg * T_max * D + sub * EPL;
 
-  for (long long f = f0 + grp; f < f1; f += NG) {
-    const int jj = (int)(f / B);
-    const int off = (int)(f % B);
-    const int j = sel[jj];
-    const int tok = j * B + off;
-    const bool valid = (j >= 0 && j <= bc && tok <= p);
-    uint4 kraw = make_uint4(0, 0, 0, 0), vraw = make_uint4(0, 0, 0, 0);
-    if (valid) {
-      kraw = *reinterpret_cast<const uint4*>(Kb + (long long)tok * D);
-      vraw = *reinterpret_cast<const uint4*>(Vb + (long long)tok * D);
-    }
-    float kf[EPL], vf[EPL];
-    if constexpr (sizeof(T) == 2) {
-      const uint32_t kw[4] = {kraw.x, kraw.y, kraw.z, kraw.w};
-      const uint32_t vw[4] = {vraw.x, vraw.y, vraw.z, vraw.w};
+  // this workgroup's slice of the selected-block list, cached in LDS
+  __shared__ int sel_sh[kDecodeSelCache];
+  const int jj0 = (int)(f0 / B);
+  const int nsh = (f1 > f0) ? (int)((f1 - 1) / B) - jj0 + 1 : 0;
+  const bool cached = nsh <= kDecodeSelCache;
+  if (cached)
+    for (int x = tid; x < nsh; x += 256) sel_sh[x] = sel[jj0 + x];
+  __syncthreads();
+
+  constexpr int U = 4;                           // tokens per key group per step
+  for (long long fb = f0 + (long long)grp * U; fb < f1; fb += (long long)NG * U) {
+    uint4 kraw[U], vraw[U];
+    bool valid[U];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        kf[2 * e] = __uint_as_float(kw[e] << 16);
-        kf[2 * e + 1] = __uint_as_float(kw[e] & 0xffff0000u);
-        vf[2 * e] = __uint_as_float(vw[e] << 16);
-        vf[2 * e + 1] = __uint_as_float(vw[e] & 0xffff0000u);
+    for (int x = 0; x < U; ++x) {
+      const long long f = fb + x;
+      bool ok2 = f < f1;
+      int tok = 0;
+      if (ok2) {
+        const int jj = (int)(f / B);
+        const int off = (int)(f - (long long)jj * B);
+        const int j = cached ? sel_sh[jj - jj0] : sel[jj];
+        tok = j * B + off;
+        ok2 = (j >= 0 && j <= bc && tok <= p);
       }
-    } else {
-      kf[0] = __uint_as_float(kraw.x); kf[1] = __uint_as_float(kraw.y);
-      kf[2] = __uint_as_float(kraw.z); kf[3] = __uint_as_float(kraw.w);
-      vf[0] = __uint_as_float(vraw.x); vf[1] = __uint_as_float(vraw.y);
-      vf[2] = __uint_as_float(vraw.z); vf[3] = __uint_as_float(vraw.w);
+      valid[x] = ok2;
+      kraw[x] = make_uint4(0, 0, 0, 0);
+      vraw[x] = make_uint4(0, 0, 0, 0);
+      if (ok2) {
+        kraw[x] = *reinterpret_cast<const uint4*>(Kb + (long long)tok * D);
+        vraw[x] = *reinterpret_cast<const uint4*>(Vb + (long long)tok * D);
+      }
     }
-    float s[G];
+    float sc[U][G];
 #pragma unroll
-    for (int u = 0; u < G; ++u) {
-      float a = 0.0f;
+    for (int x = 0; x < U; ++x) {
+      float kf[EPL];
+      if constexpr (sizeof(T) == 2) {
+        const uint32_t kw[4] = {kraw[x].x, kraw[x].y, kraw[x].z, kraw[x].w};
 #pragma unroll
-      for (int e = 0; e < EPL; ++e) a += qv[u][e] * kf[e];
-#pragma unroll
-      for (int off2 = LPK / 2; off2 > 0; off2 >>= 1) a += __shfl_xor(a, off2);
-      s[u] = valid ? a : -INFINITY;
-    }
-    if (valid) {
+        for (int e = 0; e < 4; ++e) {
+          kf[2 * e] = __uint_as_float(kw[e] << 16);
+          kf[2 * e + 1] = __uint_as_float(kw[e] & 0xffff0000u);
+        }
+      } else {
+        kf[0] = __uint_as_float(kraw[x].x); kf[1] = __uint_as_float(kraw[x].y);
+        kf[2] = __uint_as_float(kraw[x].z); kf[3] = __uint_as_float(kraw[x].w);
+      }
 #pragma unroll
       for (int u = 0; u < G; ++u) {
-        const float mnew = fmaxf(mrun[u], s[u]);
-        const float alpha = exp2f(mrun[u] - mnew);
-        const float pv = exp2f(s[u] - mnew);
-        mrun[u] = mnew;
-        lrun[u] = lrun[u] * alpha + pv;
+        float a = 0.0f;
 #pragma unroll
-        for (int e = 0; e < EPL; ++e) o[u][e] = o[u][e] * alpha + pv * vf[e];
+        for (int e = 0; e < EPL; ++e) a += qv[u][e] * kf[e];
+#pragma unroll
+        for (int off2 = LPK / 2; off2 > 0; off2 >>= 1) a += __shfl_xor(a, off2);
+        sc[x][u] = valid[x] ? a : -INFINITY;
+      }
+    }
+    float vf[U][EPL];
+#pragma unroll
+    for (int x = 0; x < U; ++x) {
+      if constexpr (sizeof(T) == 2) {
+        const uint32_t vw[4] = {vraw[x].x, vraw[x].y, vraw[x].z, vraw[x].w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          vf[x][2 * e] = __uint_as_float(vw[e] << 16);
+          vf[x][2 * e + 1] = __uint_as_float(vw[e] & 0xffff0000u);
+        }
+      } else {
+        vf[x][0] = __uint_as_float(vraw[x].x); vf[x][1] = __uint_as_float(vraw[x].y);
+        vf[x][2] = __uint_as_float(vraw[x].z); vf[x][3] = __uint_as_float(vraw[x].w);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < G; ++u) {
+      float mx = sc[0][u];
+#pragma unroll
+      for (int x = 1; x < U; ++x) mx = fmaxf(mx, sc[x][u]);
+      if (mx == -INFINITY) continue;               // no valid token in this step
+      const float mnew = fmaxf(mrun[u], mx);
+      const float alpha = exp2f(mrun[u] - mnew);
+      float pv[U];
+      float ps = 0.0f;
+#pragma unroll
+      for (int x = 0; x < U; ++x) {
+        pv[x] = exp2f(sc[x][u] - mnew);
+        ps += pv[x];
+      }
+      mrun[u] = mnew;
+      lrun[u] = lrun[u] * alpha + ps;
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) {
+        float acc = o[u][e] * alpha;
+#pragma unroll
+        for (int x = 0; x < U; ++x) acc += pv[x] * vf[x][e];
+        o[u][e] = acc;
       }
     }
   }
@@ -429,6 +526,219 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(const T* __restrict__ 
       }
     }
     const long long hu = (long long)bi * h_q + g * G + u;   // global (sequence, q head)
+    ws_o[(hu * nsp + sp) * D + dim] = Osum;
+    if (dim == 0) {
+      ws_ml[(hu * nsp + sp) * 2 + 0] = M;
+      ws_ml[(hu * nsp + sp) * 2 + 1] = Lsum;
+    }
+  }
+}
+
+// bf16 split-K decode attention on MFMA. Workgroup = (sequence, KV head,
+// split), 4 wavefronts; a wavefront takes groups of 16 consecutive selected
+// tokens (2 groups per step, all loads issued first).
+//   S = K q^T   v_mfma_f32_16x16x32_bf16: A = 16 key rows x 32 dims read
+//               straight from the cache (16 bytes per lane), B = the G query
+//               heads (zero-padded to 16 columns). Lane n + 16 (m / 4) holds
+//               key m of head n, so the online-softmax state of a head stays
+//               in the lane (plus two exchanges for the max).
+//   O^T += V^T P^T  v_mfma_f32_16x16x16bf16_1k: A = V^T from a per-wave LDS
+//               slice written transposed (4 keys x 8 dims per lane), B = P in
+//               the accumulator layout of S.
+typedef __bf16 bf16x8d __attribute__((ext_vector_type(8)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4d __attribute__((ext_vector_type(4)));
+
+template <int D>
+__global__ __launch_bounds__(256) void attn_decode_mfma_kernel(
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ Kc, const uint16_t* __restrict__ Vc,
+    int h_kv, int G, int T_max, int B, const int32_t* __restrict__ pos,
+    const int32_t* __restrict__ idx, const int32_t* __restrict__ cnt, int kmax, float sl2, int S,
+    float* __restrict__ ws) {
+  constexpr int VTS = 16 + 4;                      // V^T row stride (keys + pad)
+  constexpr int GPS = 2;                           // 16-token groups per wave step
+  // LDS: per-wave V^T slices during the loop; the epilogue's partials reuse it
+  constexpr int VT_BYTES = 4 * GPS * D * VTS * 2;
+  constexpr int EP_BYTES = (4 * 16 * D + 2 * 4 * 16) * 4;
+  __shared__ __attribute__((aligned(16))) char smem[VT_BYTES > EP_BYTES ? VT_BYTES : EP_BYTES];
+  auto vt_slice = [&](int wv, int x) {
+    return reinterpret_cast<uint16_t*>(smem) + (wv * GPS + x) * D * VTS;
+  };
+  float (*sm_o)[16][D] = reinterpret_cast<float (*)[16][D]>(smem);
+  float (*sm_m)[16] = reinterpret_cast<float (*)[16]>(smem + 4 * 16 * D * 4);
+  float (*sm_l)[16] = reinterpret_cast<float (*)[16]>(smem + 4 * 16 * D * 4 + 4 * 16 * 4);
+  const int sp = blockIdx.x % S;
+  const int bg = blockIdx.x / S;                   // (sequence, kv head)
+  const int bi = bg / h_kv;
+  const int g = bg % h_kv;
+  const int h_q = h_kv * G;
+  const int tid = threadIdx.x;
+  const int w = tid >> 6, l = tid & 63;
+  const int ln = l & 15, lg = l >> 4;
+  const int p = pos[bi];
+  const bool ok = p >= 0 && p < T_max;
+  const int bc = ok ? p / B : 0;
+  const int tau = ok ? max(0, min(cnt[bi], kmax)) : 0;
+  const int ngroups = tau * (B / 16);
+  const int g0 = (int)((long long)ngroups * sp / S), g1 = (int)((long long)ngroups * (sp + 1) / S);
+  const int32_t* sel = idx + (long long)bi * kmax;
+
+  // query fragments (B operand of S = K q^T): head ln, dims 32c + 8 lg .. +7
+  bf16x8d qf[D / 32];
+  {
+    const bool hv = ln < G;
+    const uint16_t* qp = q + ((long long)bi * h_q + g * G + (hv ? ln : 0)) * D + lg * 8;
+#pragma unroll
+    for (int c = 0; c < D / 32; ++c) {
+      uint4 v = hv ? *reinterpret_cast<const uint4*>(qp + 32 * c) : make_uint4(0, 0, 0, 0);
+      qf[c] = *reinterpret_cast<bf16x8d*>(&v);
+    }
+  }
+  f32x4d oacc[D / 16];
+#pragma unroll
+  for (int t = 0; t < D / 16; ++t) oacc[t] = f32x4d{0.f, 0.f, 0.f, 0.f};
+  float mrun = -INFINITY, lrun = 0.0f;
+  const uint16_t* Kb = Kc + (long long)bg * T_max * D;
+  const uint16_t* Vb = Vc + (long long)bg * T_max * D;
+  // V staging: lane takes keys 4 kq .. 4 kq + 3 and dims 8 dq .. 8 dq + 7
+  const int kq = l & 3, dq = l >> 2;
+  const bool vthr = dq < D / 8;
+
+  const int nsteps = (g1 - g0 + 4 * GPS - 1) / (4 * GPS);
+  for (int it = 0; it < nsteps; ++it) {
+    uint4 kraw[GPS][D / 32];
+    uint4 vraw[GPS][4];
+    int tok0[GPS];
+    bool gvalid[GPS];
+#pragma unroll
+    for (int x = 0; x < GPS; ++x) {
+      const int gi = g0 + (it * 4 + w) * GPS + x;
+      bool v = gi < g1;
+      int t0 = 0;
+      if (v) {
+        const int f = gi * 16;
+        const int jj = f / B;
+        const int j = sel[jj];
+        t0 = j * B + (f - jj * B);
+        v = (j >= 0 && j <= bc && t0 <= p);
+      }
+      gvalid[x] = v;
+      tok0[x] = t0;
+      const int key = t0 + ln;
+      const bool kv = v && key <= p;
+#pragma unroll
+      for (int c = 0; c < D / 32; ++c)
+        kraw[x][c] = kv ? *reinterpret_cast<const uint4*>(Kb + (long long)key * D + 32 * c + lg * 8)
+                        : make_uint4(0, 0, 0, 0);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int vk = t0 + kq * 4 + r;
+        vraw[x][r] = (v && vthr && vk <= p)
+                         ? *reinterpret_cast<const uint4*>(Vb + (long long)vk * D + dq * 8)
+                         : make_uint4(0, 0, 0, 0);
+      }
+    }
+    // V^T into this wave's LDS slice
+#pragma unroll
+    for (int x = 0; x < GPS; ++x) {
+      if (vthr) {
+        uint16_t* vt = vt_slice(w, x);
+        const uint32_t a[4] = {vraw[x][0].x, vraw[x][0].y, vraw[x][0].z, vraw[x][0].w};
+        const uint32_t b[4] = {vraw[x][1].x, vraw[x][1].y, vraw[x][1].z, vraw[x][1].w};
+        const uint32_t c[4] = {vraw[x][2].x, vraw[x][2].y, vraw[x][2].z, vraw[x][2].w};
+        const uint32_t d[4] = {vraw[x][3].x, vraw[x][3].y, vraw[x][3].z, vraw[x][3].w};
+#pragma unroll
+        for (int wd = 0; wd < 4; ++wd) {
+          uint2 lo, hi;
+          lo.x = (a[wd] & 0xffffu) | (b[wd] << 16);
+          lo.y = (c[wd] & 0xffffu) | (d[wd] << 16);
+          hi.x = (a[wd] >> 16) | (b[wd] & 0xffff0000u);
+          hi.y = (c[wd] >> 16) | (d[wd] & 0xffff0000u);
+          *reinterpret_cast<uint2*>(vt + (dq * 8 + 2 * wd) * VTS + kq * 4) = lo;
+          *reinterpret_cast<uint2*>(vt + (dq * 8 + 2 * wd + 1) * VTS + kq * 4) = hi;
+        }
+      }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+    for (int x = 0; x < GPS; ++x) {
+      if (!gvalid[x]) continue;                    // uniform across the wavefront
+      f32x4d sacc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int c = 0; c < D / 32; ++c)
+        sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(*reinterpret_cast<bf16x8d*>(&kraw[x][c]),
+                                                       qf[c], sacc, 0, 0, 0);
+      float sv[4];
+      float mx = -INFINITY;
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int key = tok0[x] + 4 * lg + v;
+        sv[v] = (key <= p) ? sacc[v] * sl2 : -INFINITY;
+        mx = fmaxf(mx, sv[v]);
+      }
+      mx = fmaxf(mx, __shfl_xor(mx, 16));
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      const float mnew = fmaxf(mrun, mx);          // finite: key tok0 <= p is valid
+      const float alpha = exp2f(mrun - mnew);
+      mrun = mnew;
+      float pv[4];
+      float ps = 0.0f;
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        pv[v] = exp2f(sv[v] - mnew);
+        ps += pv[v];
+      }
+      lrun = lrun * alpha + ps;
+      s16x4 pb;
+      pb[0] = (short)f32_to_bf16(pv[0]);
+      pb[1] = (short)f32_to_bf16(pv[1]);
+      pb[2] = (short)f32_to_bf16(pv[2]);
+      pb[3] = (short)f32_to_bf16(pv[3]);
+      const uint16_t* vt = vt_slice(w, x);
+#pragma unroll
+      for (int t = 0; t < D / 16; ++t) {
+        oacc[t] *= alpha;
+        const uint2 va = *reinterpret_cast<const uint2*>(vt + (t * 16 + ln) * VTS + lg * 4);
+        oacc[t] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(*reinterpret_cast<const s16x4*>(&va),
+                                                            pb, oacc[t], 0, 0, 0);
+      }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  }
+  __syncthreads();                                 // V^T slices are dead from here
+  // per-wave partials: head ln; lane groups hold disjoint keys (sum l) and
+  // disjoint output dims
+  float lsum = lrun + __shfl_xor(lrun, 16);
+  lsum += __shfl_xor(lsum, 32);
+  if (lg == 0) {
+    sm_m[w][ln] = mrun;
+    sm_l[w][ln] = lsum;
+  }
+#pragma unroll
+  for (int t = 0; t < D / 16; ++t)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) sm_o[w][ln][t * 16 + 4 * lg + v] = oacc[t][v];
+  __syncthreads();
+  const int nsp = S;
+  float* ws_ml = ws;
+  float* ws_o = ws + (long long)gridDim.x / S * G * nsp * 2;
+  for (int xx = tid; xx < G * D; xx += 256) {
+    const int u = xx / D, dim = xx % D;
+    float M = -INFINITY;
+    for (int k = 0; k < 4; ++k) M = fmaxf(M, sm_m[k][u]);
+    float Lsum = 0.0f, Osum = 0.0f;
+    if (M != -INFINITY) {
+      for (int k = 0; k < 4; ++k) {
+        const float sc = exp2f(sm_m[k][u] - M);
+        Lsum += sm_l[k][u] * sc;
+        Osum += sm_o[k][u][dim] * sc;
+      }
+    }
+    const long long hu = (long long)bi * h_q + g * G + u;
     ws_o[(hu * nsp + sp) * D + dim] = Osum;
     if (dim == 0) {
       ws_ml[(hu * nsp + sp) * 2 + 0] = M;
@@ -496,32 +806,36 @@ hipError_t launch_decode_sketch(int dtype, const void* q_new, const void* k_new,
                                 const int32_t* cols, int r, int b_max, char* state,
                                 hipStream_t st) {
   if (dtype == SW_BF16)
-    hipLaunchKernelGGL(decode_sketch_kernel<uint16_t>, dim3((unsigned)batch), dim3(256), 0, st,
+    hipLaunchKernelGGL(decode_reps_kernel<uint16_t>, dim3((unsigned)batch), dim3(256), 0, st,
                        reinterpret_cast<const uint16_t*>(q_new),
                        reinterpret_cast<const uint16_t*>(k_new), h_q, h_kv, d, B, pos, signs, cols,
                        r, batch, b_max, state);
   else
-    hipLaunchKernelGGL(decode_sketch_kernel<float>, dim3((unsigned)batch), dim3(256), 0, st,
+    hipLaunchKernelGGL(decode_reps_kernel<float>, dim3((unsigned)batch), dim3(256), 0, st,
                        reinterpret_cast<const float*>(q_new), reinterpret_cast<const float*>(k_new),
                        h_q, h_kv, d, B, pos, signs, cols, r, batch, b_max, state);
+  const int nch = (b_max + kScoreChunk - 1) / kScoreChunk;
+  hipLaunchKernelGGL(decode_scores_kernel, dim3((unsigned)batch, (unsigned)nch), dim3(256), 0, st,
+                     pos, r, B, batch, d, b_max, state);
   return hipGetLastError();
 }
 
 hipError_t launch_decode_walk(const char* state, int batch, int d, int r, int b_max, int B,
                               const int32_t* pos, int s_exp, const double* r_prev, double* r_out,
-                              double* partial, hipStream_t st) {
-  const int nch = (b_max + kWalkRowChunk - 1) / kWalkRowChunk;
-  if (r_prev != nullptr)
-    hipLaunchKernelGGL(walk_row_partial_kernel, dim3((unsigned)batch, (unsigned)nch), dim3(256), 0,
-                       st, state, batch, d, r, b_max, B, pos, s_exp, r_prev, partial);
-  hipLaunchKernelGGL(walk_row_finish_kernel, dim3((unsigned)batch), dim3(256), 0, st, state, batch,
-                     d, r, b_max, B, pos, s_exp, r_prev == nullptr ? 1 : 0, partial, r_out);
+                              hipStream_t st) {
+  const int nstrip = (b_max + kStrip - 1) / kStrip;
+  hipLaunchKernelGGL(walk_row_strip_kernel, dim3((unsigned)batch, (unsigned)nstrip), dim3(256), 0, st,
+                     state, batch, d, r, b_max, B, pos, s_exp, r_prev, r_out);
+  hipLaunchKernelGGL(walk_row_norm_kernel, dim3((unsigned)batch), dim3(256), 0, st, b_max, B, pos,
+                     r_out);
   return hipGetLastError();
 }
 
+// Splits per (sequence, KV head): about 512 workgroups, i.e. every CU once
+// at the bf16 kernel's occupancy (2 workgroups of 4 waves per CU).
 int decode_attn_splits(int batch, int h_kv) {
   const int pairs = batch * h_kv;
-  int S = (1024 + pairs - 1) / pairs;
+  int S = (512 + pairs - 1) / pairs;
   if (S < 1) S = 1;
   if (S > kDecodeMaxSplits) S = kDecodeMaxSplits;
   return S;
@@ -553,8 +867,12 @@ hipError_t launch_attn_decode(int dtype, const void* q, const void* Kc, const vo
     auto qq = reinterpret_cast<const uint16_t*>(q);
     auto kk = reinterpret_cast<const uint16_t*>(Kc);
     auto vv = reinterpret_cast<const uint16_t*>(Vc);
-    if (d == 128) launch_attn_decode_t<uint16_t, 128>(G, grid, st, qq, kk, vv, h_kv, T_max, B, pos, idx, cnt, kmax, sl2, S, ws);
-    else launch_attn_decode_t<uint16_t, 64>(G, grid, st, qq, kk, vv, h_kv, T_max, B, pos, idx, cnt, kmax, sl2, S, ws);
+    if (d == 128)
+      hipLaunchKernelGGL(attn_decode_mfma_kernel<128>, grid, dim3(256), 0, st, qq, kk, vv, h_kv, G,
+                         T_max, B, pos, idx, cnt, kmax, sl2, S, ws);
+    else
+      hipLaunchKernelGGL(attn_decode_mfma_kernel<64>, grid, dim3(256), 0, st, qq, kk, vv, h_kv, G,
+                         T_max, B, pos, idx, cnt, kmax, sl2, S, ws);
     hipLaunchKernelGGL(attn_merge_kernel<uint16_t>, dim3((unsigned)n_hu), dim3(128), 0, st, ws, S, d,
                        n_hu, reinterpret_cast<uint16_t*>(O));
   } else {

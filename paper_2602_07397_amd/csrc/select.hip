@@ -27,7 +27,7 @@ __device__ void select_row_dev(const double* __restrict__ vals, int avail, int f
                                int kmax) {
   __shared__ int hist[256];
   __shared__ int scan_tmp[256];
-  __shared__ int sh_digit, sh_need;
+  __shared__ int sh_digit, sh_need, sh_cnt;
   const int t = threadIdx.x;
   const int E = (avail + 255) / 256;
   const int nf = (first >= 0) + (last >= 0 && last != first);
@@ -53,12 +53,14 @@ __device__ void select_row_dev(const double* __restrict__ vals, int avail, int f
     }
   }
 
-  unsigned long long thr = 0ull;
-  int take_eq = 0;
+  // Radix select of the m-th largest candidate key, MSB first. After each
+  // pass the candidates matching `prefix` under `pmask` contain the boundary;
+  // the loop stops early once every candidate in the boundary bin is taken.
+  unsigned long long prefix = 0ull, pmask = 0ull;
+  int need = m;
+  bool take_all_eq = false;
   const bool partial = (m > 0 && m < nc);
   if (partial) {
-    unsigned long long prefix = 0ull, pmask = 0ull;
-    int need = m;
     for (int pass = 0; pass < 8; ++pass) {
       const int shift = 56 - 8 * pass;
       hist[t] = 0;
@@ -74,23 +76,27 @@ __device__ void select_row_dev(const double* __restrict__ vals, int avail, int f
       if (v > 0 && excl < need && need <= excl + v) {
         sh_digit = 255 - t;
         sh_need = need - excl;
+        sh_cnt = v;
       }
       __syncthreads();
       prefix |= ((unsigned long long)sh_digit) << shift;
       pmask |= 255ull << shift;
       need = sh_need;
+      const bool done = (sh_need == sh_cnt);
       __syncthreads();
+      if (done) {
+        take_all_eq = true;
+        break;
+      }
     }
-    thr = prefix;
-    take_eq = need;
   }
 
-  // rank of each threshold-valued candidate among equals, in index order
+  // rank of each boundary-valued candidate among equals, in index order
   int my_eq = 0;
-  if (partial) {
+  if (partial && !take_all_eq) {
 #pragma unroll
     for (int e = 0; e < kMaxPerThread; ++e)
-      if (((candmask >> e) & 1u) && key[e] == thr) ++my_eq;
+      if (((candmask >> e) & 1u) && (key[e] & pmask) == prefix) ++my_eq;
   }
   int dummy;
   int eq_before = block_exclusive_scan_256(my_eq, scan_tmp, &dummy);
@@ -100,10 +106,11 @@ __device__ void select_row_dev(const double* __restrict__ vals, int avail, int f
   for (int e = 0; e < kMaxPerThread; ++e) {
     if ((candmask >> e) & 1u) {
       bool take;
+      const unsigned long long kk = key[e] & pmask;
       if (m >= nc) take = true;
       else if (m <= 0) take = false;
-      else if (key[e] > thr) take = true;
-      else if (key[e] == thr) take = (eq_before++ < take_eq);
+      else if (kk > prefix) take = true;
+      else if (kk == prefix) take = take_all_eq || (eq_before++ < need);
       else take = false;
       if (take) selmask |= 1u << e;
     }

@@ -13,30 +13,33 @@ namespace sw {
 //   int32  col0[batch]           first key block whose column decode fills
 //   int32  cnt[batch][2]         token counts of the open query / key block
 //   double bar[batch][2][d]      running means of the open query / key block
+//   double qt[batch][r]          sketch of the current token's query
 //   double Qs[batch][b_max][r]   sketch of every query-block representative
 //   double Ks[batch][b_max][r]   sketch of every key-block representative
-//   float  A[batch][b_max][b_max] block-score cache
+//   float  A[batch][b_max][lda]  block-score cache, lda = b_max rounded up to 4
 struct DecodeLayout {
-  int64_t scale, col0, cnt, bar, qs, ks, a, total;
+  int64_t scale, col0, cnt, bar, qt, qs, ks, a, total;
+  int lda;
 };
 
 __host__ __device__ inline DecodeLayout decode_layout(int batch, int d, int r, int b_max) {
   auto al = [](int64_t x) { return (x + 255) / 256 * 256; };
   DecodeLayout L;
+  L.lda = (b_max + 3) & ~3;
   int64_t o = 0;
   L.scale = o; o = al(o + 8LL * batch);
   L.col0 = o;  o = al(o + 4LL * batch);
   L.cnt = o;   o = al(o + 8LL * batch);
   L.bar = o;   o = al(o + 16LL * batch * d);
+  L.qt = o;    o = al(o + 8LL * batch * r);
   L.qs = o;    o = al(o + 8LL * batch * b_max * r);
   L.ks = o;    o = al(o + 8LL * batch * b_max * r);
-  L.a = o;     o = al(o + 4LL * batch * b_max * b_max);
+  L.a = o;     o = al(o + 4LL * batch * b_max * L.lda);
   L.total = o;
   return L;
 }
 
 constexpr int kDecodeMaxSplits = 32;
-constexpr int kWalkRowChunk = 64;
 
 int64_t sketch_workspace_bytes(int h_q, int h_kv, int d, int64_t nb);
 
@@ -72,7 +75,7 @@ hipError_t launch_decode_sketch(int dtype, const void* q_new, const void* k_new,
 
 hipError_t launch_decode_walk(const char* state, int batch, int d, int r, int b_max, int B,
                               const int32_t* pos, int s_exp, const double* r_prev, double* r_out,
-                              double* partial, hipStream_t st);
+                              hipStream_t st);
 
 hipError_t launch_select_decode(const double* rows, int batch, int b_max, int B,
                                 const int32_t* pos, int k, int pct, uint32_t flags, int32_t* idx,

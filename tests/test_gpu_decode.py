@@ -54,8 +54,6 @@ class DecodeRun:
                 self.Vh[l][b] = Vf
                 self.ost[l][b] = O.decode_state_from_prefill(Q, K, self.B, self.signs, self.cols, self.b_max)
         self.kmax = sw.select_max_count_decode(self.b_max, density_pct=w.pct)
-        self.wsw = torch.empty((sw.walk_decode_workspace_bytes(self.batch, self.b_max),),
-                               dtype=torch.uint8, device=U.DEV)
         torch.cuda.synchronize()
 
     def step(self, k, check=True):
@@ -71,7 +69,7 @@ class DecodeRun:
             sw.kv_append(kd, vd, self.Kc[l], self.Vc[l], pos)
             sw.sketch_scores_decode(qd, kd, self.B, pos, self.ts, self.tc, self.b_max, self.state[l])
             r_gpu = sw.walk_update_decode(self.state[l], self.batch, w.d, w.r, self.b_max, self.B, pos,
-                                          w.s, r_prev=r_gpu, workspace=self.wsw)
+                                          w.s, r_prev=r_gpu)
             idx, cnt, _ = sw.select_topk_blocks_decode(r_gpu, self.B, pos, density_pct=w.pct,
                                                        kmax=self.kmax)
             out = sw.sparse_attn_decode(qd, self.Kc[l], self.Vc[l], self.B, pos, idx, cnt, self.kmax)
@@ -164,3 +162,76 @@ def test_first_layer_walk_row_is_power_of_score_row():
     row, _, _ = O.decode_layer_step(run.ost[0][0], q[0], k[0], 200, None, w.B, run.signs, run.cols,
                                     w.s, pct=w.pct)
     assert U.max_abs(r.cpu().numpy()[0, :200 // w.B + 1], row) <= 1e-5
+
+
+def _fixed_step_fn(run, bufs, outs):
+    """One decode step over all layers reading fixed input buffers and writing
+    per-layer outputs (so that it can be captured in a graph)."""
+    w = run.w
+    bq, bk, bv, pos = bufs
+
+    def body():
+        r = None
+        for l in range(w.layers):
+            sw.kv_append(bk[l], bv[l], run.Kc[l], run.Vc[l], pos)
+            sw.sketch_scores_decode(bq[l], bk[l], run.B, pos, run.ts, run.tc, run.b_max, run.state[l])
+            r = sw.walk_update_decode(run.state[l], run.batch, w.d, w.r, run.b_max, run.B, pos, w.s,
+                                      r_prev=r, r_out=outs["r"][l])
+            sw.select_topk_blocks_decode(r, run.B, pos, density_pct=w.pct, kmax=run.kmax,
+                                         idx=outs["idx"][l], cnt=outs["cnt"][l])
+            sw.sparse_attn_decode(bq[l], run.Kc[l], run.Vc[l], run.B, pos, outs["idx"][l],
+                                  outs["cnt"][l], run.kmax, O=outs["O"][l], workspace=outs["wsa"])
+        pos.add_(1)
+    return body
+
+
+def test_decode_graph_replay_matches_eager():
+    """A decode step captured in a HIP graph and replayed several times (with
+    eager work and synchronisation between replays) gives, at every replay,
+    the bits of the same step launched eagerly."""
+    w = _small(layers=3)
+    prompts = [300, 128, 75]
+    steps = 6
+    runs = [DecodeRun(w, prompts=prompts, steps=steps) for _ in range(2)]
+    inputs = [[synth.decode_step_inputs(w, k, l, batch=len(prompts)) for l in range(w.layers)]
+              for k in range(steps)]
+    results = []
+    for mode, run in zip(("eager", "graph"), runs):
+        bq = torch.stack([U.to_dev(inputs[0][l][0]) for l in range(w.layers)])
+        bk = torch.stack([U.to_dev(inputs[0][l][1]) for l in range(w.layers)])
+        bv = torch.stack([U.to_dev(inputs[0][l][2]) for l in range(w.layers)])
+        pos = U.to_dev(np.array(prompts, dtype=np.int32))
+        outs = {
+            "r": [torch.empty((run.batch, run.b_max), dtype=torch.float64, device=U.DEV) for _ in range(w.layers)],
+            "idx": [torch.empty((run.batch, run.kmax), dtype=torch.int32, device=U.DEV) for _ in range(w.layers)],
+            "cnt": [torch.empty((run.batch,), dtype=torch.int32, device=U.DEV) for _ in range(w.layers)],
+            "O": [torch.empty((run.batch, w.h_q, w.d), dtype=torch.bfloat16, device=U.DEV) for _ in range(w.layers)],
+            "wsa": torch.empty((sw.decode_attn_workspace_bytes(run.batch, w.h_q, w.h_kv, w.d),),
+                               dtype=torch.uint8, device=U.DEV),
+        }
+        body = _fixed_step_fn(run, (bq, bk, bv, pos), outs)
+        graph = None
+        if mode == "graph":
+            torch.cuda.synchronize()
+            graph = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(graph):
+                body()
+            torch.cuda.synchronize()
+        per_step = []
+        for k in range(steps):
+            for l in range(w.layers):
+                bq[l].copy_(U.to_dev(inputs[k][l][0]))
+                bk[l].copy_(U.to_dev(inputs[k][l][1]))
+                bv[l].copy_(U.to_dev(inputs[k][l][2]))
+            if graph is not None:
+                graph.replay()
+            else:
+                body()
+            torch.cuda.synchronize()
+            _ = (torch.ones(8, device=U.DEV) * 2).sum().item()   # eager work between replays
+            per_step.append({key: [t.clone() for t in outs[key]] for key in ("r", "idx", "cnt", "O")})
+        results.append(per_step)
+    for k in range(steps):
+        for key in ("r", "idx", "cnt", "O"):
+            for l in range(w.layers):
+                assert torch.equal(results[0][k][key][l], results[1][k][key][l]), (k, key, l)
