@@ -72,7 +72,7 @@ __device__ __forceinline__ void lpt_row(const SeqMeta& m, int rho, int* row, int
 template <int D>
 struct BfLds {
   static constexpr int KS = D + 8;     // K row stride (elements): 16-byte pad
-  static constexpr int VS = KT + 4;    // V^T row stride (elements): 8-byte pad
+  static constexpr int VS = KT + 8;    // V^T row stride (elements): 16-byte pad
   static constexpr int K_ELEMS = KT * KS;
   static constexpr int V_ELEMS = D * VS;
   static constexpr int STAGE = K_ELEMS + V_ELEMS;
@@ -148,25 +148,34 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_bf16_kernel(
     *valid = (j >= 0 && j <= i);
     *k0 = seq0 + (*valid ? j : 0) * B + kt * KT;
   };
+  // One uniform branch per tile; inside it every load is unconditional, with
+  // the key index clamped to the sequence (keys past the end are masked in
+  // the softmax and get zero probability).
   auto load_tile = [&](int t) {
     int k0;
     bool valid;
     tile_key0(t, &k0, &valid);
+    if (valid) {
+      const uint16_t* Kg = K + (long long)g * N * D;
+      const uint16_t* Vg = V + (long long)g * N * D;
 #pragma unroll
-    for (int p = 0; p < KPASS; ++p) {
-      const int e = tid + p * 256;
-      const int key = e / KCH, ch = e % KCH;
-      const int kp = k0 + key;
-      kreg[p] = (valid && kp < seq1)
-                    ? *reinterpret_cast<const uint4*>(K + ((long long)g * N + kp) * D + ch * 8)
-                    : make_uint4(0, 0, 0, 0);
-    }
+      for (int p = 0; p < KPASS; ++p) {
+        const int e = tid + p * 256;
+        const int key = e / KCH, ch = e % KCH;
+        const int kp = min(k0 + key, seq1 - 1);
+        kreg[p] = *reinterpret_cast<const uint4*>(Kg + (long long)kp * D + ch * 8);
+      }
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int kp = k0 + vkg * 4 + r;
-      vreg[r] = (vthr && valid && kp < seq1)
-                    ? *reinterpret_cast<const uint4*>(V + ((long long)g * N + kp) * D + vdg * 8)
-                    : make_uint4(0, 0, 0, 0);
+      for (int r = 0; r < 4; ++r) {
+        const int kp = min(k0 + vkg * 4 + r, seq1 - 1);
+        vreg[r] = vthr ? *reinterpret_cast<const uint4*>(Vg + (long long)kp * D + vdg * 8)
+                       : make_uint4(0, 0, 0, 0);
+      }
+    } else {
+#pragma unroll
+      for (int p = 0; p < KPASS; ++p) kreg[p] = make_uint4(0, 0, 0, 0);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) vreg[r] = make_uint4(0, 0, 0, 0);
     }
   };
   auto store_tile = [&](int buf) {
@@ -183,6 +192,11 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_bf16_kernel(
       const uint32_t b[4] = {vreg[1].x, vreg[1].y, vreg[1].z, vreg[1].w};
       const uint32_t c[4] = {vreg[2].x, vreg[2].y, vreg[2].z, vreg[2].w};
       const uint32_t d[4] = {vreg[3].x, vreg[3].y, vreg[3].z, vreg[3].w};
+      // keys vkg*4 .. +3 go to position perm(vkg*4): bits 2 and 3 of the key
+      // swapped, so that the 8 keys one lane feeds to the P.V MFMA
+      // (c*16 + hl*4 + {0..3} and c*16 + 8 + hl*4 + {0..3}) are contiguous
+      const int kb = vkg * 4;
+      const int kpos = (kb & ~12) | ((kb & 4) << 1) | ((kb & 8) >> 1);
 #pragma unroll
       for (int wd = 0; wd < 4; ++wd) {
         uint2 lo, hi;
@@ -190,8 +204,8 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_bf16_kernel(
         lo.y = (c[wd] & 0xffffu) | (d[wd] << 16);
         hi.x = (a[wd] >> 16) | (b[wd] & 0xffff0000u);
         hi.y = (c[wd] >> 16) | (d[wd] & 0xffff0000u);
-        *reinterpret_cast<uint2*>(vt + (vdg * 8 + 2 * wd) * L::VS + vkg * 4) = lo;
-        *reinterpret_cast<uint2*>(vt + (vdg * 8 + 2 * wd + 1) * L::VS + vkg * 4) = hi;
+        *reinterpret_cast<uint2*>(vt + (vdg * 8 + 2 * wd) * L::VS + kpos) = lo;
+        *reinterpret_cast<uint2*>(vt + (vdg * 8 + 2 * wd + 1) * L::VS + kpos) = hi;
       }
     }
   };
@@ -232,14 +246,15 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_bf16_kernel(
           sacc[h2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[kk], sacc[h2], 0, 0, 0);
         }
       }
-      // scale, mask, running max
+      // running max on the raw scores (the scale is positive), masking
+      // only where the tile can reach past the query or the sequence end
       const bool need_mask = (k0 + KT - 1 > q0) || (k0 + KT > seq1);
       float mx = -INFINITY;
 #pragma unroll
       for (int h2 = 0; h2 < 2; ++h2) {
 #pragma unroll
         for (int j = 0; j < 16; ++j) {
-          float v = sacc[h2][j] * sl2;
+          float v = sacc[h2][j];
           if (need_mask) {
             const int kp = k0 + h2 * 32 + (j >> 2) * 8 + hl * 4 + (j & 3);
             if (kp > qpos || kp >= seq1) v = -INFINITY;
@@ -248,10 +263,11 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_bf16_kernel(
           mx = fmaxf(mx, v);
         }
       }
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      mx = fmaxf(mx, __shfl_xor(mx, 32)) * sl2;
       const float mnew = fmaxf(mrun, mx);
       const float mref = (mnew == -INFINITY) ? 0.0f : mnew;
-      const float alpha = exp2f(mrun - mref);
+      const float alpha = __builtin_amdgcn_exp2f(mrun - mref);
+      const bool rescale = __any(mnew != mrun);   // skip the O rescale when no max moved
       mrun = mnew;
       float psum = 0.0f;
       bf16x8 pb[4];
@@ -260,7 +276,7 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_bf16_kernel(
         float pv[8];
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          pv[e] = exp2f(sacc[c >> 1][(c & 1) * 8 + e] - mref);
+          pv[e] = __builtin_amdgcn_exp2f(fmaf(sacc[c >> 1][(c & 1) * 8 + e], sl2, -mref));
           psum += pv[e];
         }
         uint32_t wds[4];
@@ -269,18 +285,19 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_bf16_kernel(
         pb[c] = *reinterpret_cast<bf16x8*>(wds);
       }
       lrun = lrun * alpha + psum;
+      if (rescale) {
+#pragma unroll
+        for (int td = 0; td < D / 32; ++td)
+#pragma unroll
+          for (int j = 0; j < 16; ++j) oacc[td][j] *= alpha;
+      }
 #pragma unroll
       for (int td = 0; td < D / 32; ++td) {
 #pragma unroll
-        for (int j = 0; j < 16; ++j) oacc[td][j] *= alpha;
-#pragma unroll
         for (int c = 0; c < 4; ++c) {
-          const uint16_t* vp = vt + (td * 32 + ln) * L::VS + c * 16 + hl * 4;
-          uint2 lo = *reinterpret_cast<const uint2*>(vp);
-          uint2 hi = *reinterpret_cast<const uint2*>(vp + 8);
-          uint4 av = make_uint4(lo.x, lo.y, hi.x, hi.y);
-          oacc[td] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<bf16x8*>(&av), pb[c],
-                                                            oacc[td], 0, 0, 0);
+          const bf16x8 av =
+              *reinterpret_cast<const bf16x8*>(vt + (td * 32 + ln) * L::VS + c * 16 + hl * 8);
+          oacc[td] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pb[c], oacc[td], 0, 0, 0);
         }
       }
     }

@@ -28,7 +28,22 @@ namespace sw {
 constexpr float kLog2eD = 1.4426950408889634f;
 constexpr int kDecodeSelCache = 512;   // selected-block entries cached per workgroup
 
+// Tuning constants (overridable at build time).
+#ifndef SW_DEC_GPS
+#define SW_DEC_GPS 2          // 16-token groups per wavefront step in decode attention
+#endif
+#ifndef SW_DEC_WGS
+#define SW_DEC_WGS 512        // target decode-attention workgroups per launch
+#endif
+#ifndef SW_STRIP_RG
+#define SW_STRIP_RG 64        // row groups per walk-row strip workgroup
+#endif
+
 __device__ __forceinline__ double pow_int_d(double x, int s) {
+  if (s == 8) {               // the paper's default exponent: three squarings
+    const double x2 = x * x, x4 = x2 * x2;
+    return x4 * x4;
+  }
   double r = 1.0, b = x;
   while (s) {
     if (s & 1) r *= b;
@@ -240,10 +255,11 @@ __global__ __launch_bounds__(256) void decode_scores_kernel(const int32_t* __res
 // walk row
 // ---------------------------------------------------------------------------
 
-constexpr int kStrip = 32;       // columns per workgroup (8 lanes x 4)
-constexpr int kRowGroups = 32;   // row groups per workgroup
+constexpr int kStrip = 32;               // columns per workgroup (8 lanes x 4)
+constexpr int kRowGroups = SW_STRIP_RG;  // row groups per workgroup
+constexpr int kStripThreads = 8 * kRowGroups;
 
-__global__ __launch_bounds__(256) void walk_row_strip_kernel(const char* __restrict__ state,
+__global__ __launch_bounds__(kStripThreads) void walk_row_strip_kernel(const char* __restrict__ state,
                                                              int batch, int d, int r, int b_max,
                                                              int B, const int32_t* __restrict__ pos,
                                                              int s_exp,
@@ -556,7 +572,7 @@ __global__ __launch_bounds__(256) void attn_decode_mfma_kernel(
     const int32_t* __restrict__ idx, const int32_t* __restrict__ cnt, int kmax, float sl2, int S,
     float* __restrict__ ws) {
   constexpr int VTS = 16 + 4;                      // V^T row stride (keys + pad)
-  constexpr int GPS = 2;                           // 16-token groups per wave step
+  constexpr int GPS = SW_DEC_GPS;                  // 16-token groups per wave step
   // LDS: per-wave V^T slices during the loop; the epilogue's partials reuse it
   constexpr int VT_BYTES = 4 * GPS * D * VTS * 2;
   constexpr int EP_BYTES = (4 * 16 * D + 2 * 4 * 16) * 4;
@@ -605,15 +621,18 @@ __global__ __launch_bounds__(256) void attn_decode_mfma_kernel(
   const bool vthr = dq < D / 8;
 
   const int nsteps = (g1 - g0 + 4 * GPS - 1) / (4 * GPS);
-  for (int it = 0; it < nsteps; ++it) {
-    uint4 kraw[GPS][D / 32];
-    uint4 vraw[GPS][4];
-    int tok0[GPS];
-    bool gvalid[GPS];
+  // Register double buffering: the loads of step it+1 are issued before the
+  // math of step it.
+  uint4 kraw[GPS][D / 32], vraw[GPS][4];
+  uint4 nk[GPS][D / 32], nvv[GPS][4];
+  int tok0[GPS], ntok[GPS];
+  bool gvalid[GPS], nvalid[GPS];
+  auto issue = [&](int step, uint4 (&kr)[GPS][D / 32], uint4 (&vr)[GPS][4], int (&t0s)[GPS],
+                   bool (&vals)[GPS]) {
 #pragma unroll
     for (int x = 0; x < GPS; ++x) {
-      const int gi = g0 + (it * 4 + w) * GPS + x;
-      bool v = gi < g1;
+      const int gi = g0 + (step * 4 + w) * GPS + x;
+      bool v = step < nsteps && gi < g1;
       int t0 = 0;
       if (v) {
         const int f = gi * 16;
@@ -622,22 +641,26 @@ __global__ __launch_bounds__(256) void attn_decode_mfma_kernel(
         t0 = j * B + (f - jj * B);
         v = (j >= 0 && j <= bc && t0 <= p);
       }
-      gvalid[x] = v;
-      tok0[x] = t0;
+      vals[x] = v;
+      t0s[x] = t0;
       const int key = t0 + ln;
       const bool kv = v && key <= p;
 #pragma unroll
       for (int c = 0; c < D / 32; ++c)
-        kraw[x][c] = kv ? *reinterpret_cast<const uint4*>(Kb + (long long)key * D + 32 * c + lg * 8)
-                        : make_uint4(0, 0, 0, 0);
+        kr[x][c] = kv ? *reinterpret_cast<const uint4*>(Kb + (long long)key * D + 32 * c + lg * 8)
+                      : make_uint4(0, 0, 0, 0);
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int vk = t0 + kq * 4 + r;
-        vraw[x][r] = (v && vthr && vk <= p)
-                         ? *reinterpret_cast<const uint4*>(Vb + (long long)vk * D + dq * 8)
-                         : make_uint4(0, 0, 0, 0);
+        vr[x][r] = (v && vthr && vk <= p)
+                       ? *reinterpret_cast<const uint4*>(Vb + (long long)vk * D + dq * 8)
+                       : make_uint4(0, 0, 0, 0);
       }
     }
+  };
+  issue(0, kraw, vraw, tok0, gvalid);
+  for (int it = 0; it < nsteps; ++it) {
+    issue(it + 1, nk, nvv, ntok, nvalid);
     // V^T into this wave's LDS slice
 #pragma unroll
     for (int x = 0; x < GPS; ++x) {
@@ -708,6 +731,15 @@ __global__ __launch_bounds__(256) void attn_decode_mfma_kernel(
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+    for (int x = 0; x < GPS; ++x) {
+#pragma unroll
+      for (int c = 0; c < D / 32; ++c) kraw[x][c] = nk[x][c];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) vraw[x][r] = nvv[x][r];
+      tok0[x] = ntok[x];
+      gvalid[x] = nvalid[x];
+    }
   }
   __syncthreads();                                 // V^T slices are dead from here
   // per-wave partials: head ln; lane groups hold disjoint keys (sum l) and
@@ -824,18 +856,18 @@ hipError_t launch_decode_walk(const char* state, int batch, int d, int r, int b_
                               const int32_t* pos, int s_exp, const double* r_prev, double* r_out,
                               hipStream_t st) {
   const int nstrip = (b_max + kStrip - 1) / kStrip;
-  hipLaunchKernelGGL(walk_row_strip_kernel, dim3((unsigned)batch, (unsigned)nstrip), dim3(256), 0, st,
+  hipLaunchKernelGGL(walk_row_strip_kernel, dim3((unsigned)batch, (unsigned)nstrip), dim3(kStripThreads), 0, st,
                      state, batch, d, r, b_max, B, pos, s_exp, r_prev, r_out);
   hipLaunchKernelGGL(walk_row_norm_kernel, dim3((unsigned)batch), dim3(256), 0, st, b_max, B, pos,
                      r_out);
   return hipGetLastError();
 }
 
-// Splits per (sequence, KV head): about 512 workgroups, i.e. every CU once
-// at the bf16 kernel's occupancy (2 workgroups of 4 waves per CU).
+// Splits per (sequence, KV head): about SW_DEC_WGS workgroups; 512 fills
+// every CU once at the bf16 kernel's occupancy (2 workgroups of 4 waves).
 int decode_attn_splits(int batch, int h_kv) {
   const int pairs = batch * h_kv;
-  int S = (512 + pairs - 1) / pairs;
+  int S = (SW_DEC_WGS + pairs - 1) / pairs;
   if (S < 1) S = 1;
   if (S > kDecodeMaxSplits) S = kDecodeMaxSplits;
   return S;

@@ -16,6 +16,10 @@ namespace sw {
 typedef double f64x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ double pow_int(double x, int s) {
+  if (s == 8) {               // the paper's default exponent: three squarings
+    const double x2 = x * x, x4 = x2 * x2;
+    return x4 * x4;
+  }
   double r = 1.0, b = x;
   while (s) {
     if (s & 1) r *= b;
