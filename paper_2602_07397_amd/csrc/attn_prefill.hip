@@ -78,7 +78,10 @@ struct BfLds {
   static constexpr int STAGE = K_ELEMS + V_ELEMS;
 };
 
-template <int D>
+// Raw buffer descriptor word 3 for gfx9-family untyped loads (32-bit data format).
+constexpr int kBufWord3 = 0x00020000;
+
+template <int D, int BLK>
 __global__ __launch_bounds__(256, 2) void attn_prefill_bf16_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
     const uint16_t* __restrict__ V, int h_q, int h_kv, long long N, SeqMeta m,
@@ -98,14 +101,14 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_bf16_kernel(
   const int g = gamma % h_kv;
   int row, s, i;
   lpt_row(m, rho, &row, &s, &i);
-  const int B = m.B;
+  constexpr int B = BLK;
   const int G = h_q / h_kv;
   const int tid = threadIdx.x;
   const int w = tid >> 6;
   const int l = tid & 63;
   const int hl = l >> 5;            // half-wave
   const int ln = l & 31;            // lane within half
-  const int hpw = (B == 64) ? 2 : 1;  // query heads per workgroup
+  constexpr int hpw = (B == 64) ? 2 : 1;  // query heads per workgroup
   const int u = g * G + mu * hpw + (hpw == 2 ? (w >> 1) : 0);
   const int rw = (hpw == 2) ? (w & 1) : w;   // 32-row slice within the block
   const int seq0 = m.tok_start[s];
@@ -129,7 +132,7 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_bf16_kernel(
   // ---- selected block list ----
   const int nsel = min(cnt[row], kmax);
   const int32_t* sel = idx + (long long)row * kmax;
-  const int tpb = B / KT;                  // key tiles per block
+  constexpr int tpb = B / KT;              // key tiles per block
   const int ntiles = nsel * tpb;
 
   // global -> register staging for one tile
@@ -148,28 +151,38 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_bf16_kernel(
     *valid = (j >= 0 && j <= i);
     *k0 = seq0 + (*valid ? j : 0) * B + kt * KT;
   };
-  // One uniform branch per tile; inside it every load is unconditional, with
-  // the key index clamped to the sequence (keys past the end are masked in
-  // the softmax and get zero probability).
+  // One uniform branch per tile. The loads are raw buffer loads through a
+  // descriptor based at the tile's first key and sized to the end of the
+  // sequence, so keys past the end read as zero without any per-lane test
+  // (they are masked in the softmax); per-lane offsets are tile invariant.
+  const uint16_t* Kg = K + (long long)g * N * D;
+  const uint16_t* Vg = V + (long long)g * N * D;
+  int koff[KPASS];
+#pragma unroll
+  for (int p = 0; p < KPASS; ++p) {
+    const int e = tid + p * 256;
+    koff[p] = (e / KCH) * D * 2 + (e % KCH) * 16;
+  }
+  const int voff = (vkg * 4 * D + vdg * 8) * 2;
   auto load_tile = [&](int t) {
     int k0;
     bool valid;
     tile_key0(t, &k0, &valid);
     if (valid) {
-      const uint16_t* Kg = K + (long long)g * N * D;
-      const uint16_t* Vg = V + (long long)g * N * D;
+      const int bytes = max(0, (seq1 - k0) * D * 2);   // 0: every load returns zero
+      const __amdgpu_buffer_rsrc_t rk =
+          __builtin_amdgcn_make_buffer_rsrc((void*)(Kg + (long long)k0 * D), (short)0, bytes, kBufWord3);
+      const __amdgpu_buffer_rsrc_t rv =
+          __builtin_amdgcn_make_buffer_rsrc((void*)(Vg + (long long)k0 * D), (short)0, bytes, kBufWord3);
 #pragma unroll
       for (int p = 0; p < KPASS; ++p) {
-        const int e = tid + p * 256;
-        const int key = e / KCH, ch = e % KCH;
-        const int kp = min(k0 + key, seq1 - 1);
-        kreg[p] = *reinterpret_cast<const uint4*>(Kg + (long long)kp * D + ch * 8);
+        auto v = __builtin_amdgcn_raw_buffer_load_b128(rk, koff[p], 0, 0);
+        kreg[p] = *reinterpret_cast<uint4*>(&v);
       }
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int kp = min(k0 + vkg * 4 + r, seq1 - 1);
-        vreg[r] = vthr ? *reinterpret_cast<const uint4*>(Vg + (long long)kp * D + vdg * 8)
-                       : make_uint4(0, 0, 0, 0);
+        auto v = __builtin_amdgcn_raw_buffer_load_b128(rv, voff + r * D * 2, 0, 0);
+        vreg[r] = vthr ? *reinterpret_cast<uint4*>(&v) : make_uint4(0, 0, 0, 0);
       }
     } else {
 #pragma unroll
@@ -231,7 +244,7 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_bf16_kernel(
     int k0;
     bool valid;
     tile_key0(t, &k0, &valid);
-    if (active && valid && k0 <= q0 + 31) {
+    if (active && valid && k0 <= q0 + 31 && k0 < seq1) {
       const uint16_t* ks = lds + (t & 1) * L::STAGE;
       const uint16_t* vt = ks + L::K_ELEMS;
       f32x16 sacc[2];
@@ -493,12 +506,14 @@ hipError_t launch_attn_prefill(int dtype, const void* Q, const void* K, const vo
     auto k = reinterpret_cast<const uint16_t*>(K);
     auto v = reinterpret_cast<const uint16_t*>(V);
     auto o = reinterpret_cast<uint16_t*>(O);
-    if (d == 128)
-      hipLaunchKernelGGL(attn_prefill_bf16_kernel<128>, dim3(grid), dim3(256), 0, st, q, k, v, h_q,
-                         h_kv, N, meta, idx, cnt, kmax, sl2, o, lse, groups, sg);
-    else
-      hipLaunchKernelGGL(attn_prefill_bf16_kernel<64>, dim3(grid), dim3(256), 0, st, q, k, v, h_q,
-                         h_kv, N, meta, idx, cnt, kmax, sl2, o, lse, groups, sg);
+#define SW_LAUNCH_BF16(DD, BB)                                                                  \
+  hipLaunchKernelGGL((attn_prefill_bf16_kernel<DD, BB>), dim3(grid), dim3(256), 0, st, q, k, v, h_q, \
+                     h_kv, N, meta, idx, cnt, kmax, sl2, o, lse, groups, sg)
+    if (d == 128 && meta.B == 128) SW_LAUNCH_BF16(128, 128);
+    else if (d == 128) SW_LAUNCH_BF16(128, 64);
+    else if (meta.B == 128) SW_LAUNCH_BF16(64, 128);
+    else SW_LAUNCH_BF16(64, 64);
+#undef SW_LAUNCH_BF16
   } else {
     auto q = reinterpret_cast<const float*>(Q);
     auto k = reinterpret_cast<const float*>(K);
