@@ -1,0 +1,215 @@
+"""GPU parity at the workloads' full sizes, in the launch configuration the
+benchmark times. The oracle checks every selection row and a sample of the
+attention outputs (whole query blocks for sampled (head, block) pairs; the
+oracle computes them one by one)."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import synth
+from paper_2602_07397_amd import binding as sw
+
+pytestmark = pytest.mark.gpu
+
+U = pytest.importorskip("_gpu_util")
+
+
+def _sample_blocks(b, rng, n_random):
+    picks = {0, b - 1, b // 2}
+    picks |= set(int(x) for x in rng.integers(0, b, size=n_random))
+    return sorted(picks)
+
+
+def _check_attention_sample(Qh, Kh, Vh, Og, B, sel_rows, pairs):
+    """Oracle sparse attention for sampled (head, query block) pairs, given
+    the GPU's selection; returns the max abs error."""
+    err = 0.0
+    for (u, i) in pairs:
+        ref = O.sparse_attention_block(Qh, Kh, Vh, B, sel_rows[i], u, i)
+        got = Og[u, i * B:i * B + ref.shape[0]]
+        err = max(err, U.max_abs(got, ref))
+    return err
+
+
+def _to_host(*ts):
+    return [O.f64(t) for t in ts]
+
+
+def test_llama8b_layers_full_size():
+    """Llama-3-8B-shaped prefill (32/8 heads, d=128, n=32768, B=128, 20%),
+    8 consecutive walked layers."""
+    w = synth.WORKLOADS["llama8b"]
+    signs, cols, ts, tc = U.srht_dev(w.d, w.r, w.seed)
+    cu = synth.cu_seqlens(w.seqlens)
+    rng = np.random.default_rng(7)
+    R_gpu, R_ref = None, None
+    near_total, rows_total, worst = 0, 0, 0.0
+    for layer in range(8):
+        Q, K, V = synth.prefill_layer_inputs(w, layer, device=U.DEV)
+        res = U.gpu_prefill_layer(Q, K, V, cu, w.B, ts, tc, w.s, R_gpu, pct=w.pct)
+        R_gpu = res["R"]
+        Qh, Kh, Vh = _to_host(Q, K, V)
+        ref = O.prefill_layer(Qh, Kh, Vh, w.B, signs, cols, w.s, R_ref, pct=w.pct, attention=False)
+        R_ref = ref["R"]
+        got = U.gpu_selection(res["idx"], res["cnt"])
+        near_total += U.check_selection(got, ref["sel"], ref["gaps"], R_ref)
+        rows_total += len(got)
+        b = len(got)
+        pairs = [(int(rng.integers(w.h_q)), i) for i in _sample_blocks(b, rng, 5)]
+        Og = res["O"].float().cpu().numpy()
+        worst = max(worst, _check_attention_sample(Qh, Kh, Vh, Og, w.B, got, pairs))
+        del Qh, Kh, Vh, Og
+    assert worst <= U.ATOL_BF16, worst
+    assert near_total <= 0.05 * rows_total, (near_total, rows_total)
+
+
+@pytest.mark.parametrize("pct", synth.STRESS_DENSITIES)
+def test_stress_layer_density_sweep(pct):
+    """One layer, 32/8 heads, n=131072, B=128; density 100% must equal dense
+    causal attention."""
+    w = synth.WORKLOADS["stress"]
+    signs, cols, ts, tc = U.srht_dev(w.d, w.r, w.seed)
+    cu = synth.cu_seqlens(w.seqlens)
+    Q, K, V = synth.prefill_layer_inputs(w, 0, device=U.DEV)
+    res = U.gpu_prefill_layer(Q, K, V, cu, w.B, ts, tc, w.s, None, pct=pct)
+    got = U.gpu_selection(res["idx"], res["cnt"])
+    b = len(got)
+    # selection: the oracle's selection path on the full layer
+    Qa = O.head_mean(Q.float().cpu())
+    Ka = O.head_mean(K.float().cpu())
+    Qs = O.srht(O.block_means(Qa, w.B), signs, cols)
+    Ks = O.srht(O.block_means(Ka, w.B), signs, cols)
+    A = O.block_scores(Qs, Ks)
+    R = O.walk_step(None, O.walk_weights(A, O.score_scale(A), w.s))
+    sel, gaps = O.select_blocks(R, pct=pct)
+    near = U.check_selection(got, sel, gaps, R)
+    assert near <= 0.05 * b
+    if pct == 100:
+        assert got == [list(range(i + 1)) for i in range(b)]
+    # attention on sampled blocks, whole query blocks (dense when pct = 100)
+    rng = np.random.default_rng(pct)
+    pairs = [(int(rng.integers(w.h_q)), i) for i in _sample_blocks(b, rng, 3)]
+    Og = res["O"]
+    err = 0.0
+    G = w.h_q // w.h_kv
+    for (u, i) in pairs:
+        g = u // G
+        lo, hi = i * w.B, (i + 1) * w.B
+        # one query head and its KV head, tokens up to the end of block i
+        ref = O.sparse_attention_block(O.f64(Q[u:u + 1, :hi].cpu()), O.f64(K[g:g + 1, :hi].cpu()),
+                                       O.f64(V[g:g + 1, :hi].cpu()), w.B, got[i], 0, i)
+        err = max(err, U.max_abs(Og[u, lo:hi].float().cpu().numpy(), ref))
+    assert err <= U.ATOL_BF16, err
+
+
+def test_varlen_batch_full_size():
+    """8 sequences of lengths in [8192, 131072], 28/4 heads, d=128, B=128,
+    log-normal key-block scales, 2 walked layers. Selection is checked on
+    every row of the shortest, the longest and one middle sequence."""
+    w = synth.WORKLOADS["varlen"]
+    signs, cols, ts, tc = U.srht_dev(w.d, w.r, w.seed)
+    cu = synth.cu_seqlens(w.seqlens)
+    order = np.argsort(w.seqlens)
+    check = sorted({int(order[0]), int(order[-1]), int(order[len(order) // 2])})
+    R_gpu = None
+    R_ref = {s: None for s in check}
+    rng = np.random.default_rng(11)
+    for layer in range(w.layers):
+        Q, K, V = synth.prefill_layer_inputs(w, layer, device=U.DEV)
+        res = U.gpu_prefill_layer(Q, K, V, cu, w.B, ts, tc, w.s, R_gpu, pct=w.pct)
+        R_gpu = res["R"]
+        got_all = U.gpu_selection(res["idx"], res["cnt"])
+        rows = U.split_rows(np.arange(len(got_all)), cu, w.B)
+        for s in check:
+            a, e = int(cu[s]), int(cu[s + 1])
+            Qh = O.f64(Q[:, a:e].cpu())
+            Kh = O.f64(K[:, a:e].cpu())
+            ref = O.prefill_layer(Qh, Kh, None, w.B, signs, cols, w.s, R_ref[s], pct=w.pct,
+                                  attention=False)
+            R_ref[s] = ref["R"]
+            got = [got_all[r] for r in rows[s]]
+            near = U.check_selection(got, ref["sel"], ref["gaps"], ref["R"])
+            assert near <= 0.05 * len(got) + 1
+            Vh = O.f64(V[:, a:e].cpu())
+            b = len(got)
+            pairs = [(int(rng.integers(w.h_q)), i) for i in _sample_blocks(b, rng, 2)]
+            Og = res["O"][:, a:e].float().cpu().numpy()
+            err = _check_attention_sample(Qh, Kh, Vh, Og, w.B, got, pairs)
+            assert err <= U.ATOL_BF16, (layer, s, err)
+            del Qh, Kh, Vh, Og
+
+
+def test_decode_full_size_sampled():
+    """Decode at batch 16 with 65536-token caches (32/8 heads, B=64, 20%):
+    the GPU runs the whole batch through 4 walked layers for 3 steps; the
+    oracle follows sequences 0 and 15."""
+    w = synth.scaled(synth.WORKLOADS["decode"], layers=4)
+    batch, n0, B = w.batch, w.kv_len, w.B
+    steps = 3
+    T_max = n0 + steps
+    b_max = -(-T_max // B)
+    signs, cols, ts, tc = U.srht_dev(w.d, w.r, w.seed)
+    follow = (0, batch - 1)
+    L = w.layers
+    Kc = [torch.empty((batch, w.h_kv, T_max, w.d), dtype=torch.bfloat16, device=U.DEV) for _ in range(L)]
+    Vc = [torch.empty_like(Kc[0]) for _ in range(L)]
+    state = [sw.new_decode_state(batch, w.d, w.r, b_max, U.DEV) for _ in range(L)]
+    ost = {}
+    Kh = {}
+    Vh = {}
+    for l in range(L):
+        for b in range(batch):
+            Q, K, V = synth.decode_prefix_inputs(w, l, b, device=U.DEV)
+            sk = sw.sketch_scores(Q, K, [0, n0], B, ts, tc, want_means=True)
+            sw.decode_state_init(state[l], batch, w.d, w.r, b_max, b, n0, B, sk)
+            Kc[l][b, :, :n0] = K
+            Vc[l][b, :, :n0] = V
+            if b in follow:
+                ost[(l, b)] = O.decode_state_from_prefill(Q.cpu(), K.cpu(), B, signs, cols, b_max)
+                kf = np.zeros((w.h_kv, T_max, w.d))
+                vf = np.zeros((w.h_kv, T_max, w.d))
+                kf[:, :n0] = O.f64(K.cpu())
+                vf[:, :n0] = O.f64(V.cpu())
+                Kh[(l, b)] = kf
+                Vh[(l, b)] = vf
+    kmax = sw.select_max_count_decode(b_max, density_pct=w.pct)
+    werr, aerr, near, rows = 0.0, 0.0, 0, 0
+    for k in range(steps):
+        pos_h = np.full((batch,), n0 + k, dtype=np.int32)
+        pos = U.to_dev(pos_h)
+        r_gpu = None
+        r_ref = {b: None for b in follow}
+        for l in range(L):
+            q, kk, v = synth.decode_step_inputs(w, k, l, device=U.DEV)
+            sw.kv_append(kk, v, Kc[l], Vc[l], pos)
+            sw.sketch_scores_decode(q, kk, B, pos, ts, tc, b_max, state[l])
+            r_gpu = sw.walk_update_decode(state[l], batch, w.d, w.r, b_max, B, pos, w.s, r_prev=r_gpu)
+            idx, cnt, _ = sw.select_topk_blocks_decode(r_gpu, B, pos, density_pct=w.pct, kmax=kmax)
+            out = sw.sparse_attn_decode(q, Kc[l], Vc[l], B, pos, idx, cnt, kmax)
+            got = U.gpu_selection(idx, cnt)
+            rg = r_gpu.cpu().numpy()
+            og = out.float().cpu().numpy()
+            qh, kh, vh = O.f64(q.cpu()), O.f64(kk.cpu()), O.f64(v.cpu())
+            p = n0 + k
+            bc = p // B
+            for b in follow:
+                Kh[(l, b)][:, p] = kh[b]
+                Vh[(l, b)][:, p] = vh[b]
+                row, sel, gap = O.decode_layer_step(ost[(l, b)], qh[b], kh[b], p, r_ref[b], B, signs,
+                                                    cols, w.s, pct=w.pct)
+                r_ref[b] = row
+                werr = max(werr, U.max_abs(rg[b, :bc + 1], row))
+                rows += 1
+                if gap > U.GAP_TOL:
+                    assert got[b] == sel, (k, l, b)
+                else:
+                    near += 1
+                    assert len(got[b]) == len(sel) and {0, bc} <= set(got[b])
+                ref = O.decode_attention(qh[b], Kh[(l, b)], Vh[(l, b)], got[b], p, B)
+                aerr = max(aerr, U.max_abs(og[b], ref))
+    assert werr <= 1e-4, werr
+    assert aerr <= U.ATOL_BF16, aerr
+    assert near <= max(1, 0.1 * rows), (near, rows)
