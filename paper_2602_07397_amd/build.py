@@ -24,6 +24,14 @@ HIPFLAGS = [
     "-Wall", "-Wno-unused-result",
 ]
 
+# Per-source extras. The prefill attention kernel runs one 512-register
+# wavefront per SIMD; MFMA results it post-processes on the VALU (scores) must
+# land in VGPRs, while staging and long-lived operands go to AGPRs: the VGPR
+# form of the MFMA instructions lets the register allocator do that split.
+EXTRA = {
+    "attn_prefill.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
+}
+
 
 def _hipcc() -> str:
     for cand in (shutil.which("hipcc"), "/opt/rocm/bin/hipcc"):
@@ -34,7 +42,7 @@ def _hipcc() -> str:
 
 def _compile(src: str) -> str:
     obj = os.path.join(OBJDIR, os.path.basename(src) + ".o")
-    cmd = [_hipcc(), *HIPFLAGS, "-c", src, "-o", obj]
+    cmd = [_hipcc(), *HIPFLAGS, *EXTRA.get(os.path.basename(src), []), "-c", src, "-o", obj]
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         raise RuntimeError(f"hipcc failed for {src}:\n{res.stderr}")

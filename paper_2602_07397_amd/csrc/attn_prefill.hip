@@ -3,33 +3,54 @@
 // the tokens of the selected blocks that precede each query, renormalised
 // over those keys only.
 //
-// Work item = (query block, KV head g, query-head slice). A 256-thread
-// workgroup has 4 wavefronts of 32 query rows each: with B = 128 they are the
-// 128 rows of one query head; with B = 64 they are two query heads of the same
-// KV group. All waves share the K/V tiles staged in LDS.
+// bf16 kernel. Work item = (query block, KV head g, slice of the group's query
+// heads). A 256-thread workgroup has 4 wavefronts; each owns 64 query rows
+// (one head; a B = 128 block takes two wavefronts per head, a B = 64 block
+// one), so a workgroup serves two (B = 128) or four (B = 64) query heads of
+// the same KV group from one copy of each K/V tile in LDS. One wavefront per
+// SIMD with the full 512-entry register file: the 64-row tile halves the LDS
+// bytes read per MFMA compared with 32-row wavefronts.
 //
 // Per wavefront and 64-key tile the scores are computed transposed,
-// S^T = K Q^T, so that each lane owns one query column: the running max and
-// sum stay in the lane plus one exchange with the other half-wave. P then
-// feeds the B operand of O^T = V^T P^T directly from the accumulator layout;
-// V is staged transposed in LDS so that the A operand is two 8-byte reads.
-//   bf16:  v_mfma_f32_32x32x16_bf16, fp32 accumulate, P rounded to bf16.
-//   fp32:  v_mfma_f32_32x32x2f32, P kept in fp32.
-// Tiles are double-buffered in LDS; the next tile's global loads are issued
-// before the current tile's math. Work items run longest-first (query blocks
-// in descending order, the selection budget grows with the block index) and
-// the workgroups of one (query block, KV head) are placed on one XCD so they
-// share the K/V blocks through that XCD's L2.
+// S^T = K Q^T (v_mfma_f32_32x32x16_bf16, fp32 accumulate), so a lane owns one
+// query column: its running max and sum stay in the lane plus one
+// v_permlane32_swap with the other half-wave. P (rounded to bf16) feeds the B
+// operand of O^T = V^T P^T straight from the accumulator layout. V stays in
+// its natural row layout in LDS and the V^T operand is read with
+// ds_read_b64_tr_b16, which hands each lane four consecutive keys of one
+// dimension.
+//
+// Software pipeline over tiles: while the exponentials of tile t run on the
+// VALU, the MFMAs compute the scores of tile t+1; the row max of t+1 is taken
+// during the P.V MFMAs of tile t. K/V tiles go through three LDS stages from
+// registers loaded one tile ahead. The exponent reference of a row moves only
+// when its max grows by more than kRescaleSlack (log2 units), so the O
+// rescale is rare; P then stays below 2^kRescaleSlack.
+//
+// The selected blocks are compacted in LDS at the start: valid blocks j < i
+// first (never masked: only a sequence's last block can be partial), then the
+// diagonal block i, whose tiles apply the causal and sequence-end masks.
+// Work items run longest-first (query blocks in descending order, the
+// selection budget grows with the block index) and the workgroups of one
+// (query block, KV head) are placed on one XCD so they share the K/V blocks
+// through that XCD's L2.
+#include <type_traits>
+
 #include "sw_common.h"
 #include "sw_internal.h"
 
 namespace sw {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef short i16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 constexpr int KT = 64;                 // keys per LDS tile
 constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kRescaleSlack = 8.0f;  // log2 units
+constexpr float kNoRef = -1.0e30f;     // exponent reference before any key
 
 // ---------------------------------------------------------------------------
 // work mapping
@@ -71,24 +92,37 @@ __device__ __forceinline__ void lpt_row(const SeqMeta& m, int rho, int* row, int
 
 template <int D>
 struct BfLds {
-  static constexpr int KS = D + 8;     // K row stride (elements): 16-byte pad
-  static constexpr int VS = KT + 8;    // V^T row stride (elements): 16-byte pad
+  static constexpr int KS = D + 8;     // K row stride (elements): rows 16 bytes apart in bank space
+  static constexpr int VS = D + 32;    // V row stride (elements): rows 64 bytes apart in bank space
   static constexpr int K_ELEMS = KT * KS;
-  static constexpr int V_ELEMS = D * VS;
+  static constexpr int V_ELEMS = KT * VS;
   static constexpr int STAGE = K_ELEMS + V_ELEMS;
+  static constexpr int NST = 3;
 };
 
 // Raw buffer descriptor word 3 for gfx9-family untyped loads (32-bit data format).
 constexpr int kBufWord3 = 0x00020000;
 
+__device__ __forceinline__ float max_other_half(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float sum_other_half(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 template <int D, int BLK>
-__global__ __launch_bounds__(256, 2) void attn_prefill_bf16_kernel(
+__global__ __launch_bounds__(256, 1) void attn_prefill_bf16_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
     const uint16_t* __restrict__ V, int h_q, int h_kv, long long N, SeqMeta m,
     const int32_t* __restrict__ idx, const int32_t* __restrict__ cnt, int kmax, float sl2,
     uint16_t* __restrict__ O, float* __restrict__ lse, int groups, int sg) {
   using L = BfLds<D>;
-  __shared__ __attribute__((aligned(16))) uint16_t lds[2 * L::STAGE];
+  __shared__ __attribute__((aligned(16))) uint16_t lds[L::NST * L::STAGE];
+  __shared__ int blist[SW_MAX_BLOCKS];
+  __shared__ int wtot[4];
+  __shared__ int sdiag;
 
   // ---- work item ----
   const int x = blockIdx.x;
@@ -101,241 +135,315 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_bf16_kernel(
   const int g = gamma % h_kv;
   int row, s, i;
   lpt_row(m, rho, &row, &s, &i);
-  constexpr int B = BLK;
+  constexpr int WPB = BLK / 64;            // wavefronts per (query head, block)
+  constexpr int TPB = BLK / KT;            // key tiles per block
   const int G = h_q / h_kv;
   const int tid = threadIdx.x;
   const int w = tid >> 6;
   const int l = tid & 63;
-  const int hl = l >> 5;            // half-wave
-  const int ln = l & 31;            // lane within half
-  constexpr int hpw = (B == 64) ? 2 : 1;  // query heads per workgroup
-  const int u = g * G + mu * hpw + (hpw == 2 ? (w >> 1) : 0);
-  const int rw = (hpw == 2) ? (w & 1) : w;   // 32-row slice within the block
+  const int hl = l >> 5;                   // half-wave
+  const int ln = l & 31;                   // lane within half
+  const int task = mu * 4 + w;
+  const int u = g * G + task / WPB;        // query head (meaningful only when active)
   const int seq0 = m.tok_start[s];
   const int seq1 = m.tok_start[s + 1];
-  const int q0 = seq0 + i * B + rw * 32;     // first query token of this wave
-  const bool active = (u < (g + 1) * G) && (q0 < seq1);
+  const int q0 = seq0 + i * BLK + (task % WPB) * 64;   // first query row of this wavefront
+  const bool active = (task < G * WPB) && (q0 < seq1);
 
-  // ---- Q fragments: lane holds query q0+ln, dims kk*16 + hl*8 .. +7 ----
-  bf16x8 qf[D / 16];
-  {
-    const int qp = q0 + ln;
+  // ---- Q fragments: lane holds query q0 + qh*32 + ln, dims kk*16 + hl*8 .. +7 ----
+  bf16x8 qf[2][D / 16];
+#pragma unroll
+  for (int qh = 0; qh < 2; ++qh) {
+    const int qp = q0 + qh * 32 + ln;
     const bool ok = active && qp < seq1;
-    const uint16_t* qrow = Q + ((long long)u * N + (ok ? qp : 0)) * D;
+    const uint16_t* qrow = Q + ((long long)(ok ? u : 0) * N + (ok ? qp : 0)) * D;
 #pragma unroll
     for (int kk = 0; kk < D / 16; ++kk) {
       uint4 v = ok ? *reinterpret_cast<const uint4*>(qrow + kk * 16 + hl * 8) : make_uint4(0, 0, 0, 0);
-      qf[kk] = *reinterpret_cast<bf16x8*>(&v);
+      qf[qh][kk] = *reinterpret_cast<bf16x8*>(&v);
     }
   }
 
-  // ---- selected block list ----
+  // ---- selected blocks, compacted: valid j < i in list order, then i ----
   const int nsel = min(cnt[row], kmax);
   const int32_t* sel = idx + (long long)row * kmax;
-  constexpr int tpb = B / KT;              // key tiles per block
-  const int ntiles = nsel * tpb;
+  if (tid == 0) sdiag = 0;
+  __syncthreads();
+  int n_off = 0;
+  for (int base = 0; base < nsel; base += 256) {
+    const int e = base + tid;
+    const int j = (e < nsel) ? sel[e] : -1;
+    const bool off = (j >= 0 && j < i);
+    if (j == i) sdiag = 1;
+    const unsigned long long bal = __ballot(off);
+    const int pre = __popcll(bal & ((1ull << l) - 1ull));
+    if (l == 0) wtot[w] = __popcll(bal);
+    __syncthreads();
+    int woff = 0, tot = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      woff += (q < w) ? wtot[q] : 0;
+      tot += wtot[q];
+    }
+    if (off && n_off + woff + pre < SW_MAX_BLOCKS) blist[n_off + woff + pre] = j;
+    n_off = min(n_off + tot, SW_MAX_BLOCKS);
+    __syncthreads();
+  }
+  __syncthreads();
+  const int n_blk = n_off + sdiag;
+  const int ntiles = n_blk * TPB;
+  const int nofft = n_off * TPB;           // tiles before the diagonal block
 
-  // global -> register staging for one tile
-  constexpr int KCH = D / 8;               // 16-byte chunks per key row
-  constexpr int KPASS = (KT * KCH) / 256;  // K loads per thread
-  uint4 kreg[KPASS];
-  uint4 vreg[4];
-  const int vkg = tid & 15;                // V: keys vkg*4 .. +3
-  const int vdg = tid >> 4;                // V: dims vdg*8 .. +7
-  const bool vthr = vdg < D / 8;
-
-  auto tile_key0 = [&](int t, int* k0, bool* valid) {
-    const int jj = t / tpb;
-    const int kt = t % tpb;
-    const int j = sel[jj];
-    *valid = (j >= 0 && j <= i);
-    *k0 = seq0 + (*valid ? j : 0) * B + kt * KT;
-  };
-  // One uniform branch per tile. The loads are raw buffer loads through a
-  // descriptor based at the tile's first key and sized to the end of the
-  // sequence, so keys past the end read as zero without any per-lane test
-  // (they are masked in the softmax); per-lane offsets are tile invariant.
+  // ---- K/V staging: global -> registers -> LDS, 16-byte chunks ----
+  constexpr int KCH = D / 8;               // chunks per key row
+  constexpr int KP = (KT * KCH) / 256;     // chunks per thread for K (and for V)
+  uint4 kreg[KP], vreg[KP];
+  int goff[KP], kloff[KP], vloff[KP];
+#pragma unroll
+  for (int p = 0; p < KP; ++p) {
+    const int e = tid + p * 256;
+    const int r = e / KCH, ch = e % KCH;
+    goff[p] = (r * D + ch * 8) * 2;
+    kloff[p] = r * L::KS + ch * 8;
+    vloff[p] = r * L::VS + ch * 8;
+  }
   const uint16_t* Kg = K + (long long)g * N * D;
   const uint16_t* Vg = V + (long long)g * N * D;
-  int koff[KPASS];
-#pragma unroll
-  for (int p = 0; p < KPASS; ++p) {
-    const int e = tid + p * 256;
-    koff[p] = (e / KCH) * D * 2 + (e % KCH) * 16;
-  }
-  const int voff = (vkg * 4 * D + vdg * 8) * 2;
+  auto tile_k0 = [&](int t) {
+    const int jj = t / TPB;
+    const int j = (jj < n_off) ? blist[jj] : i;
+    return seq0 + j * BLK + (t % TPB) * KT;
+  };
+  // Raw buffer loads through a descriptor based at the tile's first key and
+  // sized to the end of the sequence: keys past the end read as zero without
+  // per-lane tests (the diagonal-tile mask removes them).
   auto load_tile = [&](int t) {
-    int k0;
-    bool valid;
-    tile_key0(t, &k0, &valid);
-    if (valid) {
-      const int bytes = max(0, (seq1 - k0) * D * 2);   // 0: every load returns zero
-      const __amdgpu_buffer_rsrc_t rk =
-          __builtin_amdgcn_make_buffer_rsrc((void*)(Kg + (long long)k0 * D), (short)0, bytes, kBufWord3);
-      const __amdgpu_buffer_rsrc_t rv =
-          __builtin_amdgcn_make_buffer_rsrc((void*)(Vg + (long long)k0 * D), (short)0, bytes, kBufWord3);
+    const int k0 = tile_k0(t);
+    const int bytes = max(0, (seq1 - k0) * D * 2);
+    const __amdgpu_buffer_rsrc_t rk =
+        __builtin_amdgcn_make_buffer_rsrc((void*)(Kg + (long long)k0 * D), (short)0, bytes, kBufWord3);
+    const __amdgpu_buffer_rsrc_t rv =
+        __builtin_amdgcn_make_buffer_rsrc((void*)(Vg + (long long)k0 * D), (short)0, bytes, kBufWord3);
 #pragma unroll
-      for (int p = 0; p < KPASS; ++p) {
-        auto v = __builtin_amdgcn_raw_buffer_load_b128(rk, koff[p], 0, 0);
-        kreg[p] = *reinterpret_cast<uint4*>(&v);
-      }
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        auto v = __builtin_amdgcn_raw_buffer_load_b128(rv, voff + r * D * 2, 0, 0);
-        vreg[r] = vthr ? *reinterpret_cast<uint4*>(&v) : make_uint4(0, 0, 0, 0);
-      }
-    } else {
-#pragma unroll
-      for (int p = 0; p < KPASS; ++p) kreg[p] = make_uint4(0, 0, 0, 0);
-#pragma unroll
-      for (int r = 0; r < 4; ++r) vreg[r] = make_uint4(0, 0, 0, 0);
+    for (int p = 0; p < KP; ++p) {
+      auto a = __builtin_amdgcn_raw_buffer_load_b128(rk, goff[p], 0, 0);
+      kreg[p] = *reinterpret_cast<uint4*>(&a);
+      auto b = __builtin_amdgcn_raw_buffer_load_b128(rv, goff[p], 0, 0);
+      vreg[p] = *reinterpret_cast<uint4*>(&b);
     }
   };
-  auto store_tile = [&](int buf) {
-    uint16_t* ks = lds + buf * L::STAGE;
-    uint16_t* vt = ks + L::K_ELEMS;
+  auto store_tile = [&](int st) {
+    uint16_t* ks = lds + st * L::STAGE;
+    uint16_t* vs = ks + L::K_ELEMS;
 #pragma unroll
-    for (int p = 0; p < KPASS; ++p) {
-      const int e = tid + p * 256;
-      const int key = e / KCH, ch = e % KCH;
-      *reinterpret_cast<uint4*>(ks + key * L::KS + ch * 8) = kreg[p];
-    }
-    if (vthr) {
-      const uint32_t a[4] = {vreg[0].x, vreg[0].y, vreg[0].z, vreg[0].w};
-      const uint32_t b[4] = {vreg[1].x, vreg[1].y, vreg[1].z, vreg[1].w};
-      const uint32_t c[4] = {vreg[2].x, vreg[2].y, vreg[2].z, vreg[2].w};
-      const uint32_t d[4] = {vreg[3].x, vreg[3].y, vreg[3].z, vreg[3].w};
-      // keys vkg*4 .. +3 go to position perm(vkg*4): bits 2 and 3 of the key
-      // swapped, so that the 8 keys one lane feeds to the P.V MFMA
-      // (c*16 + hl*4 + {0..3} and c*16 + 8 + hl*4 + {0..3}) are contiguous
-      const int kb = vkg * 4;
-      const int kpos = (kb & ~12) | ((kb & 4) << 1) | ((kb & 8) >> 1);
-#pragma unroll
-      for (int wd = 0; wd < 4; ++wd) {
-        uint2 lo, hi;
-        lo.x = (a[wd] & 0xffffu) | (b[wd] << 16);
-        lo.y = (c[wd] & 0xffffu) | (d[wd] << 16);
-        hi.x = (a[wd] >> 16) | (b[wd] & 0xffff0000u);
-        hi.y = (c[wd] >> 16) | (d[wd] & 0xffff0000u);
-        *reinterpret_cast<uint2*>(vt + (vdg * 8 + 2 * wd) * L::VS + kpos) = lo;
-        *reinterpret_cast<uint2*>(vt + (vdg * 8 + 2 * wd + 1) * L::VS + kpos) = hi;
-      }
+    for (int p = 0; p < KP; ++p) {
+      *reinterpret_cast<uint4*>(ks + kloff[p]) = kreg[p];
+      *reinterpret_cast<uint4*>(vs + vloff[p]) = vreg[p];
     }
   };
 
   // ---- running state ----
-  f32x16 oacc[D / 32];
+  f32x16 oacc[2][D / 32];
 #pragma unroll
-  for (int t = 0; t < D / 32; ++t)
+  for (int qh = 0; qh < 2; ++qh)
 #pragma unroll
-    for (int j = 0; j < 16; ++j) oacc[t][j] = 0.0f;
-  float mrun = -INFINITY;
-  float lrun = 0.0f;
-  const int qpos = q0 + ln;
+    for (int td = 0; td < D / 32; ++td)
+#pragma unroll
+      for (int j = 0; j < 16; ++j) oacc[qh][td][j] = 0.0f;
+  float mref[2] = {kNoRef, kNoRef};
+  float lsum[2] = {0.0f, 0.0f};
+  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+
+  // S^T of 32 keys (half h2 of a 64-key tile) x 64 queries: S[qh][h2] holds
+  // keys h2*32 + ..., queries qh*32 + ...
+  auto qk_half = [&](const uint16_t* ks, auto h2c, f32x16 (&S)[2][2]) {
+    constexpr int h2 = decltype(h2c)::value;
+#pragma unroll
+    for (int qh = 0; qh < 2; ++qh)
+#pragma unroll
+      for (int j = 0; j < 16; ++j) S[qh][h2][j] = 0.0f;
+#pragma unroll
+    for (int kk = 0; kk < D / 16; ++kk) {
+      const bf16x8 a = *reinterpret_cast<const bf16x8*>(ks + (h2 * 32 + ln) * L::KS + kk * 16 + hl * 8);
+      S[0][h2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[0][kk], S[0][h2], 0, 0, 0);
+      S[1][h2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[1][kk], S[1][h2], 0, 0, 0);
+    }
+  };
+  // causal + sequence-end mask of a diagonal-block tile (raw scores)
+  auto mask_tile = [&](int t, f32x16 (&S)[2][2]) {
+    const int k0 = tile_k0(t);
+#pragma unroll
+    for (int qh = 0; qh < 2; ++qh) {
+      const int qpos = q0 + qh * 32 + ln;
+#pragma unroll
+      for (int h2 = 0; h2 < 2; ++h2)
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+          const int kp = k0 + h2 * 32 + (j >> 2) * 8 + hl * 4 + (j & 3);
+          if (kp > qpos || kp >= seq1) S[qh][h2][j] = -INFINITY;
+        }
+    }
+  };
+  // row max of a tile (scaled to log2 units); moves the exponent reference
+  // of rows whose max grew by more than the slack, rescaling O and the sums
+  auto update_ref = [&](f32x16 (&S)[2][2]) {
+    float mx[2];
+#pragma unroll
+    for (int qh = 0; qh < 2; ++qh) {
+      float a = -INFINITY;
+#pragma unroll
+      for (int h2 = 0; h2 < 2; ++h2)
+#pragma unroll
+        for (int j = 0; j < 16; ++j) a = fmaxf(a, S[qh][h2][j]);
+      mx[qh] = max_other_half(a) * sl2;
+    }
+    const bool n0 = mx[0] > mref[0] + kRescaleSlack;
+    const bool n1 = mx[1] > mref[1] + kRescaleSlack;
+    if (__any(n0 || n1)) {
+#pragma unroll
+      for (int qh = 0; qh < 2; ++qh) {
+        const float nref = (qh ? n1 : n0) ? mx[qh] : mref[qh];
+        const float alpha = __builtin_amdgcn_exp2f(mref[qh] - nref);
+        mref[qh] = nref;
+        lsum[qh] *= alpha;
+#pragma unroll
+        for (int td = 0; td < D / 32; ++td)
+#pragma unroll
+          for (int j = 0; j < 16; ++j) oacc[qh][td][j] *= alpha;
+      }
+    }
+  };
+  // P = exp2(S*sl2 - ref) for key half h2 (chunks c = 2*h2, 2*h2+1), rounded
+  // to bf16; the row sums accumulate the rounded values
+  auto softmax_half = [&](f32x16 (&S)[2][2], auto h2c, bf16x8 (&pb)[2][4]) {
+    constexpr int h2 = decltype(h2c)::value;
+#pragma unroll
+    for (int qh = 0; qh < 2; ++qh) {
+      const float nr = -mref[qh];
+#pragma unroll
+      for (int cc = 0; cc < 2; ++cc) {
+        uint32_t wds[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float p0 = __builtin_amdgcn_exp2f(fmaf(S[qh][h2][cc * 8 + 2 * e], sl2, nr));
+          const float p1 = __builtin_amdgcn_exp2f(fmaf(S[qh][h2][cc * 8 + 2 * e + 1], sl2, nr));
+          wds[e] = pack_bf16x2(p0, p1);
+          lsum[qh] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, wds[e]), ones, lsum[qh], false);
+        }
+        pb[qh][h2 * 2 + cc] = __builtin_bit_cast(bf16x8, wds);
+      }
+    }
+  };
+  // O^T += V^T P^T for the chunks [C0, C1) of 16 keys. Lane (ln, hl) reads
+  // with ds_read_b64_tr_b16 from key row c*16 + 4*hl + (ln%16)/4 (+8) and
+  // dims td*32 + 16*(ln/16) + 4*(ln%4): it receives dim td*32 + ln of keys
+  // c*16 + 4*hl + 0..3 and c*16 + 8 + 4*hl + 0..3, the keys its P operand holds.
+  const int vlane = (4 * hl + ((ln & 15) >> 2)) * L::VS + 16 * (ln >> 4) + 4 * (ln & 3);
+  auto pv = [&](const uint16_t* vs, const bf16x8 (&pb)[2][4], auto c0c, auto c1c) {
+    constexpr int C0 = decltype(c0c)::value, C1 = decltype(c1c)::value;
+#pragma unroll
+    for (int c = C0; c < C1; ++c)
+#pragma unroll
+      for (int td = 0; td < D / 32; ++td) {
+        const uint16_t* p = vs + vlane + c * 16 * L::VS + td * 32;
+        const i16x4 r0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (__attribute__((address_space(3))) i16x4*)(p));
+        const i16x4 r1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (__attribute__((address_space(3))) i16x4*)(p + 8 * L::VS));
+        const i16x8 rr = __builtin_shufflevector(r0, r1, 0, 1, 2, 3, 4, 5, 6, 7);
+        const bf16x8 av = __builtin_bit_cast(bf16x8, rr);
+        oacc[0][td] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pb[0][c], oacc[0][td], 0, 0, 0);
+        oacc[1][td] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pb[1][c], oacc[1][td], 0, 0, 0);
+      }
+  };
+  using I0 = std::integral_constant<int, 0>;
+  using I1 = std::integral_constant<int, 1>;
+  using I2 = std::integral_constant<int, 2>;
+  using I4 = std::integral_constant<int, 4>;
+
+  // stages: V(t) in stv, K(t+1) in stk, tile t+2 written to stw during step t
+  int stv = 0, stk = 1, stw = 2;
+  // one pipeline step: P(t) and O += P(t) V(t), S(t+1) = K(t+1) Q^T, its max
+  auto step = [&](int t, f32x16 (&cur)[2][2], f32x16 (&nxt)[2][2]) {
+    if (t + 2 < ntiles) store_tile(stw);
+    if (t + 3 < ntiles) load_tile(t + 3);
+    const uint16_t* ks = lds + stk * L::STAGE;
+    const uint16_t* vs = lds + stv * L::STAGE + L::K_ELEMS;
+    bf16x8 pb[2][4];
+    softmax_half(cur, I0{}, pb);
+    qk_half(ks, I0{}, nxt);
+    softmax_half(cur, I1{}, pb);
+    qk_half(ks, I1{}, nxt);
+    pv(vs, pb, I0{}, I4{});
+    if (t + 1 >= nofft) mask_tile(t + 1, nxt);
+    update_ref(nxt);
+    const int t0 = stv;
+    stv = stk;
+    stk = stw;
+    stw = t0;
+    __syncthreads();
+  };
+  auto last = [&](f32x16 (&cur)[2][2]) {
+    const uint16_t* vs = lds + stv * L::STAGE + L::K_ELEMS;
+    bf16x8 pb[2][4];
+    softmax_half(cur, I0{}, pb);
+    softmax_half(cur, I1{}, pb);
+    pv(vs, pb, I0{}, I4{});
+  };
 
   if (ntiles > 0) {
     load_tile(0);
     store_tile(0);
-  }
-  __syncthreads();
-
-  for (int t = 0; t < ntiles; ++t) {
-    if (t + 1 < ntiles) load_tile(t + 1);
-    int k0;
-    bool valid;
-    tile_key0(t, &k0, &valid);
-    if (active && valid && k0 <= q0 + 31 && k0 < seq1) {
-      const uint16_t* ks = lds + (t & 1) * L::STAGE;
-      const uint16_t* vt = ks + L::K_ELEMS;
-      f32x16 sacc[2];
-#pragma unroll
-      for (int h2 = 0; h2 < 2; ++h2) {
-#pragma unroll
-        for (int j = 0; j < 16; ++j) sacc[h2][j] = 0.0f;
-#pragma unroll
-        for (int kk = 0; kk < D / 16; ++kk) {
-          const bf16x8 a =
-              *reinterpret_cast<const bf16x8*>(ks + (h2 * 32 + ln) * L::KS + kk * 16 + hl * 8);
-          sacc[h2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[kk], sacc[h2], 0, 0, 0);
-        }
-      }
-      // running max on the raw scores (the scale is positive), masking
-      // only where the tile can reach past the query or the sequence end
-      const bool need_mask = (k0 + KT - 1 > q0) || (k0 + KT > seq1);
-      float mx = -INFINITY;
-#pragma unroll
-      for (int h2 = 0; h2 < 2; ++h2) {
-#pragma unroll
-        for (int j = 0; j < 16; ++j) {
-          float v = sacc[h2][j];
-          if (need_mask) {
-            const int kp = k0 + h2 * 32 + (j >> 2) * 8 + hl * 4 + (j & 3);
-            if (kp > qpos || kp >= seq1) v = -INFINITY;
-          }
-          sacc[h2][j] = v;
-          mx = fmaxf(mx, v);
-        }
-      }
-      mx = fmaxf(mx, __shfl_xor(mx, 32)) * sl2;
-      const float mnew = fmaxf(mrun, mx);
-      const float mref = (mnew == -INFINITY) ? 0.0f : mnew;
-      const float alpha = __builtin_amdgcn_exp2f(mrun - mref);
-      const bool rescale = __any(mnew != mrun);   // skip the O rescale when no max moved
-      mrun = mnew;
-      float psum = 0.0f;
-      bf16x8 pb[4];
-#pragma unroll
-      for (int c = 0; c < 4; ++c) {
-        float pv[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          pv[e] = __builtin_amdgcn_exp2f(fmaf(sacc[c >> 1][(c & 1) * 8 + e], sl2, -mref));
-          psum += pv[e];
-        }
-        uint32_t wds[4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) wds[e] = pack_bf16x2(pv[2 * e], pv[2 * e + 1]);
-        pb[c] = *reinterpret_cast<bf16x8*>(wds);
-      }
-      lrun = lrun * alpha + psum;
-      if (rescale) {
-#pragma unroll
-        for (int td = 0; td < D / 32; ++td)
-#pragma unroll
-          for (int j = 0; j < 16; ++j) oacc[td][j] *= alpha;
-      }
-#pragma unroll
-      for (int td = 0; td < D / 32; ++td) {
-#pragma unroll
-        for (int c = 0; c < 4; ++c) {
-          const bf16x8 av =
-              *reinterpret_cast<const bf16x8*>(vt + (td * 32 + ln) * L::VS + c * 16 + hl * 8);
-          oacc[td] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pb[c], oacc[td], 0, 0, 0);
-        }
-      }
+    if (ntiles > 1) {
+      load_tile(1);
+      store_tile(1);
     }
-    if (t + 1 < ntiles) store_tile((t + 1) & 1);
+    if (ntiles > 2) load_tile(2);
     __syncthreads();
+    f32x16 sA[2][2], sB[2][2];
+    qk_half(lds, I0{}, sA);
+    qk_half(lds, I1{}, sA);
+    if (nofft == 0) mask_tile(0, sA);
+    update_ref(sA);
+    int t = 0;
+    for (; t + 2 < ntiles; t += 2) {
+      step(t, sA, sB);
+      step(t + 1, sB, sA);
+    }
+    if (t + 1 < ntiles) {
+      step(t, sA, sB);
+      last(sB);
+    } else {
+      last(sA);
+    }
   }
 
   // ---- epilogue ----
-  if (!active || qpos >= seq1) return;
-  const float ltot = lrun + __shfl_xor(lrun, 32);
-  const float inv = ltot > 0.0f ? 1.0f / ltot : 0.0f;
-  uint16_t* orow = O + ((long long)u * N + qpos) * D;
+  float ltot[2];
 #pragma unroll
-  for (int td = 0; td < D / 32; ++td) {
+  for (int qh = 0; qh < 2; ++qh) ltot[qh] = sum_other_half(lsum[qh]);
+  if (!active) return;
 #pragma unroll
-    for (int jb = 0; jb < 4; ++jb) {
-      const int dv = td * 32 + jb * 8 + hl * 4;
-      uint2 st;
-      st.x = pack_bf16x2(oacc[td][jb * 4 + 0] * inv, oacc[td][jb * 4 + 1] * inv);
-      st.y = pack_bf16x2(oacc[td][jb * 4 + 2] * inv, oacc[td][jb * 4 + 3] * inv);
-      *reinterpret_cast<uint2*>(orow + dv) = st;
+  for (int qh = 0; qh < 2; ++qh) {
+    const int qpos = q0 + qh * 32 + ln;
+    if (qpos >= seq1) continue;
+    const float inv = ltot[qh] > 0.0f ? 1.0f / ltot[qh] : 0.0f;
+    uint16_t* orow = O + ((long long)u * N + qpos) * D;
+#pragma unroll
+    for (int td = 0; td < D / 32; ++td) {
+#pragma unroll
+      for (int jb = 0; jb < 4; ++jb) {
+        const int dv = td * 32 + jb * 8 + hl * 4;
+        uint2 st;
+        st.x = pack_bf16x2(oacc[qh][td][jb * 4 + 0] * inv, oacc[qh][td][jb * 4 + 1] * inv);
+        st.y = pack_bf16x2(oacc[qh][td][jb * 4 + 2] * inv, oacc[qh][td][jb * 4 + 3] * inv);
+        *reinterpret_cast<uint2*>(orow + dv) = st;
+      }
     }
+    if (lse && hl == 0)
+      lse[(long long)u * N + qpos] =
+          (ltot[qh] > 0.0f) ? (mref[qh] + log2f(ltot[qh])) / kLog2e : -INFINITY;
   }
-  if (lse && hl == 0)
-    lse[(long long)u * N + qpos] = (ltot > 0.0f) ? (mrun + log2f(ltot)) / kLog2e : -INFINITY;
 }
 
 // ---------------------------------------------------------------------------
@@ -496,12 +604,12 @@ hipError_t launch_attn_prefill(int dtype, const void* Q, const void* K, const vo
                                const int32_t* idx, const int32_t* cnt, int kmax, float scale,
                                void* O, float* lse, hipStream_t st) {
   const int G = h_q / h_kv;
-  const int hpw = (meta.B == 64) ? 2 : 1;
-  const int sg = (G + hpw - 1) / hpw;
   const int groups = (int)(nb * h_kv);
-  const unsigned grid = (unsigned)(((groups + 7) / 8) * 8 * sg);
   const float sl2 = scale * kLog2e;
   if (dtype == SW_BF16) {
+    // 64 query rows per wavefront, 4 wavefronts per workgroup
+    const int sg = (G * (meta.B / 64) + 3) / 4;
+    const unsigned grid = (unsigned)(((groups + 7) / 8) * 8 * sg);
     auto q = reinterpret_cast<const uint16_t*>(Q);
     auto k = reinterpret_cast<const uint16_t*>(K);
     auto v = reinterpret_cast<const uint16_t*>(V);
@@ -515,6 +623,9 @@ hipError_t launch_attn_prefill(int dtype, const void* Q, const void* K, const vo
     else SW_LAUNCH_BF16(64, 64);
 #undef SW_LAUNCH_BF16
   } else {
+    const int hpw = (meta.B == 64) ? 2 : 1;
+    const int sg = (G + hpw - 1) / hpw;
+    const unsigned grid = (unsigned)(((groups + 7) / 8) * 8 * sg);
     auto q = reinterpret_cast<const float*>(Q);
     auto k = reinterpret_cast<const float*>(K);
     auto v = reinterpret_cast<const float*>(V);
