@@ -52,6 +52,7 @@ constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kRescaleSlack = 8.0f;  // log2 units
 constexpr float kNoRef = -1.0e30f;     // exponent reference before any key
 
+
 // ---------------------------------------------------------------------------
 // work mapping
 // ---------------------------------------------------------------------------
@@ -209,7 +210,7 @@ __global__ __launch_bounds__(256, 1) void attn_prefill_bf16_kernel(
   }
   const uint16_t* Kg = K + (long long)g * N * D;
   const uint16_t* Vg = V + (long long)g * N * D;
-  auto tile_k0 = [&](int t) {
+  auto tile_k0 = [&](int t) __attribute__((always_inline)) {
     const int jj = t / TPB;
     const int j = (jj < n_off) ? blist[jj] : i;
     return seq0 + j * BLK + (t % TPB) * KT;
@@ -217,7 +218,7 @@ __global__ __launch_bounds__(256, 1) void attn_prefill_bf16_kernel(
   // Raw buffer loads through a descriptor based at the tile's first key and
   // sized to the end of the sequence: keys past the end read as zero without
   // per-lane tests (the diagonal-tile mask removes them).
-  auto load_tile = [&](int t) {
+  auto load_tile = [&](int t) __attribute__((always_inline)) {
     const int k0 = tile_k0(t);
     const int bytes = max(0, (seq1 - k0) * D * 2);
     const __amdgpu_buffer_rsrc_t rk =
@@ -232,7 +233,7 @@ __global__ __launch_bounds__(256, 1) void attn_prefill_bf16_kernel(
       vreg[p] = *reinterpret_cast<uint4*>(&b);
     }
   };
-  auto store_tile = [&](int st) {
+  auto store_tile = [&](int st) __attribute__((always_inline)) {
     uint16_t* ks = lds + st * L::STAGE;
     uint16_t* vs = ks + L::K_ELEMS;
 #pragma unroll
@@ -254,49 +255,47 @@ __global__ __launch_bounds__(256, 1) void attn_prefill_bf16_kernel(
   float lsum[2] = {0.0f, 0.0f};
   const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
 
-  // S^T of 32 keys (half h2 of a 64-key tile) x 64 queries: S[qh][h2] holds
-  // keys h2*32 + ..., queries qh*32 + ...
-  auto qk_half = [&](const uint16_t* ks, auto h2c, f32x16 (&S)[2][2]) {
-    constexpr int h2 = decltype(h2c)::value;
+  // Scores of 32 keys (half h2 of a 64-key tile) x 64 queries, transposed:
+  // S[qh] element j is key h2*32 + 8*(j/4) + 4*hl + j%4, query qh*32 + ln.
+  auto qk_sub = [&](const uint16_t* ks, int h2, f32x16 (&S)[2]) __attribute__((always_inline)) {
 #pragma unroll
     for (int qh = 0; qh < 2; ++qh)
 #pragma unroll
-      for (int j = 0; j < 16; ++j) S[qh][h2][j] = 0.0f;
+      for (int j = 0; j < 16; ++j) S[qh][j] = 0.0f;
+    const uint16_t* kr = ks + (h2 * 32 + ln) * L::KS + hl * 8;
 #pragma unroll
     for (int kk = 0; kk < D / 16; ++kk) {
-      const bf16x8 a = *reinterpret_cast<const bf16x8*>(ks + (h2 * 32 + ln) * L::KS + kk * 16 + hl * 8);
-      S[0][h2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[0][kk], S[0][h2], 0, 0, 0);
-      S[1][h2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[1][kk], S[1][h2], 0, 0, 0);
+      const bf16x8 a = *reinterpret_cast<const bf16x8*>(kr + kk * 16);
+      S[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[0][kk], S[0], 0, 0, 0);
+      S[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[1][kk], S[1], 0, 0, 0);
     }
   };
-  // causal + sequence-end mask of a diagonal-block tile (raw scores)
-  auto mask_tile = [&](int t, f32x16 (&S)[2][2]) {
-    const int k0 = tile_k0(t);
+  // causal + sequence-end mask of a diagonal-block half tile (raw scores)
+  auto mask_sub = [&](int t, int h2, f32x16 (&S)[2]) __attribute__((always_inline)) {
+    const int k0 = tile_k0(t) + h2 * 32;
 #pragma unroll
     for (int qh = 0; qh < 2; ++qh) {
       const int qpos = q0 + qh * 32 + ln;
 #pragma unroll
-      for (int h2 = 0; h2 < 2; ++h2)
-#pragma unroll
-        for (int j = 0; j < 16; ++j) {
-          const int kp = k0 + h2 * 32 + (j >> 2) * 8 + hl * 4 + (j & 3);
-          if (kp > qpos || kp >= seq1) S[qh][h2][j] = -INFINITY;
-        }
+      for (int j = 0; j < 16; ++j) {
+        const int kp = k0 + (j >> 2) * 8 + hl * 4 + (j & 3);
+        if (kp > qpos || kp >= seq1) S[qh][j] = -INFINITY;
+      }
     }
   };
-  // row max of a tile (scaled to log2 units); moves the exponent reference
-  // of rows whose max grew by more than the slack, rescaling O and the sums
-  auto update_ref = [&](f32x16 (&S)[2][2]) {
-    float mx[2];
+  // row max (log2 units)
+  auto row_max = [&](f32x16 (&S)[2], float (&mx)[2]) __attribute__((always_inline)) {
 #pragma unroll
     for (int qh = 0; qh < 2; ++qh) {
       float a = -INFINITY;
 #pragma unroll
-      for (int h2 = 0; h2 < 2; ++h2)
-#pragma unroll
-        for (int j = 0; j < 16; ++j) a = fmaxf(a, S[qh][h2][j]);
+      for (int j = 0; j < 16; ++j) a = fmaxf(a, S[qh][j]);
       mx[qh] = max_other_half(a) * sl2;
     }
+  };
+  // moves the exponent reference of rows whose max grew by more than the
+  // slack, rescaling O and the sums (rare: a wave-uniform branch)
+  auto apply_ref = [&](const float (&mx)[2]) __attribute__((always_inline)) {
     const bool n0 = mx[0] > mref[0] + kRescaleSlack;
     const bool n1 = mx[1] > mref[1] + kRescaleSlack;
     if (__any(n0 || n1)) {
@@ -313,10 +312,14 @@ __global__ __launch_bounds__(256, 1) void attn_prefill_bf16_kernel(
       }
     }
   };
-  // P = exp2(S*sl2 - ref) for key half h2 (chunks c = 2*h2, 2*h2+1), rounded
-  // to bf16; the row sums accumulate the rounded values
-  auto softmax_half = [&](f32x16 (&S)[2][2], auto h2c, bf16x8 (&pb)[2][4]) {
-    constexpr int h2 = decltype(h2c)::value;
+  auto update_ref = [&](f32x16 (&S)[2]) __attribute__((always_inline)) {
+    float mx[2];
+    row_max(S, mx);
+    apply_ref(mx);
+  };
+  // P = exp2(S*sl2 - ref) for 32 keys (two 16-key chunks), rounded to bf16;
+  // the row sums accumulate the rounded values
+  auto softmax_sub = [&](f32x16 (&S)[2], bf16x8 (&pb)[2][2]) __attribute__((always_inline)) {
 #pragma unroll
     for (int qh = 0; qh < 2; ++qh) {
       const float nr = -mref[qh];
@@ -325,70 +328,179 @@ __global__ __launch_bounds__(256, 1) void attn_prefill_bf16_kernel(
         uint32_t wds[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const float p0 = __builtin_amdgcn_exp2f(fmaf(S[qh][h2][cc * 8 + 2 * e], sl2, nr));
-          const float p1 = __builtin_amdgcn_exp2f(fmaf(S[qh][h2][cc * 8 + 2 * e + 1], sl2, nr));
+          const float p0 = __builtin_amdgcn_exp2f(fmaf(S[qh][cc * 8 + 2 * e], sl2, nr));
+          const float p1 = __builtin_amdgcn_exp2f(fmaf(S[qh][cc * 8 + 2 * e + 1], sl2, nr));
           wds[e] = pack_bf16x2(p0, p1);
           lsum[qh] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, wds[e]), ones, lsum[qh], false);
         }
-        pb[qh][h2 * 2 + cc] = __builtin_bit_cast(bf16x8, wds);
+        pb[qh][cc] = __builtin_bit_cast(bf16x8, wds);
       }
     }
   };
-  // O^T += V^T P^T for the chunks [C0, C1) of 16 keys. Lane (ln, hl) reads
-  // with ds_read_b64_tr_b16 from key row c*16 + 4*hl + (ln%16)/4 (+8) and
-  // dims td*32 + 16*(ln/16) + 4*(ln%4): it receives dim td*32 + ln of keys
+  // O^T += V^T P^T for the 16-key chunks c0, c0+1 of a tile. Lane (ln, hl)
+  // reads with ds_read_b64_tr_b16 from key row c*16 + 4*hl + (ln%16)/4 (+8)
+  // and dims td*32 + 16*(ln/16) + 4*(ln%4): it receives dim td*32 + ln of keys
   // c*16 + 4*hl + 0..3 and c*16 + 8 + 4*hl + 0..3, the keys its P operand holds.
   const int vlane = (4 * hl + ((ln & 15) >> 2)) * L::VS + 16 * (ln >> 4) + 4 * (ln & 3);
-  auto pv = [&](const uint16_t* vs, const bf16x8 (&pb)[2][4], auto c0c, auto c1c) {
-    constexpr int C0 = decltype(c0c)::value, C1 = decltype(c1c)::value;
+  auto pv_sub = [&](const uint16_t* vs, const bf16x8 (&pb)[2][2], int c0) __attribute__((always_inline)) {
 #pragma unroll
-    for (int c = C0; c < C1; ++c)
+    for (int cc = 0; cc < 2; ++cc)
 #pragma unroll
       for (int td = 0; td < D / 32; ++td) {
-        const uint16_t* p = vs + vlane + c * 16 * L::VS + td * 32;
+        const uint16_t* p = vs + vlane + (c0 + cc) * 16 * L::VS + td * 32;
         const i16x4 r0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
             (__attribute__((address_space(3))) i16x4*)(p));
         const i16x4 r1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
             (__attribute__((address_space(3))) i16x4*)(p + 8 * L::VS));
         const i16x8 rr = __builtin_shufflevector(r0, r1, 0, 1, 2, 3, 4, 5, 6, 7);
         const bf16x8 av = __builtin_bit_cast(bf16x8, rr);
-        oacc[0][td] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pb[0][c], oacc[0][td], 0, 0, 0);
-        oacc[1][td] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pb[1][c], oacc[1][td], 0, 0, 0);
+        oacc[0][td] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pb[0][cc], oacc[0][td], 0, 0, 0);
+        oacc[1][td] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pb[1][cc], oacc[1][td], 0, 0, 0);
       }
   };
-  using I0 = std::integral_constant<int, 0>;
-  using I1 = std::integral_constant<int, 1>;
-  using I2 = std::integral_constant<int, 2>;
-  using I4 = std::integral_constant<int, 4>;
 
-  // stages: V(t) in stv, K(t+1) in stk, tile t+2 written to stw during step t
+  // Stages: during tile step t, K/V(t) are in stv, K(t+1) in stk, and tile
+  // t+2 is written to stw from the registers loaded during step t-1; tile
+  // t+3 is loaded into those registers.
   int stv = 0, stk = 1, stw = 2;
-  // one pipeline step: P(t) and O += P(t) V(t), S(t+1) = K(t+1) Q^T, its max
-  auto step = [&](int t, f32x16 (&cur)[2][2], f32x16 (&nxt)[2][2]) {
+  auto stage_io = [&](int t) __attribute__((always_inline)) {
     if (t + 2 < ntiles) store_tile(stw);
     if (t + 3 < ntiles) load_tile(t + 3);
-    const uint16_t* ks = lds + stk * L::STAGE;
-    const uint16_t* vs = lds + stv * L::STAGE + L::K_ELEMS;
-    bf16x8 pb[2][4];
-    softmax_half(cur, I0{}, pb);
-    qk_half(ks, I0{}, nxt);
-    softmax_half(cur, I1{}, pb);
-    qk_half(ks, I1{}, nxt);
-    pv(vs, pb, I0{}, I4{});
-    if (t + 1 >= nofft) mask_tile(t + 1, nxt);
-    update_ref(nxt);
+  };
+  auto next_stage = [&]() __attribute__((always_inline)) {
     const int t0 = stv;
     stv = stk;
     stk = stw;
     stw = t0;
     __syncthreads();
   };
-  auto last = [&](f32x16 (&cur)[2][2]) {
-    const uint16_t* vs = lds + stv * L::STAGE + L::K_ELEMS;
-    bf16x8 pb[2][4];
-    softmax_half(cur, I0{}, pb);
-    softmax_half(cur, I1{}, pb);
-    pv(vs, pb, I0{}, I4{});
+  // Pipeline sub-step over 32 keys: P of the current half and its P.V while
+  // the scores of the next half run on the MFMAs; the next half's row max
+  // overlaps the P.V MFMAs.
+  // One pipeline sub-step over 32 keys, written as a fixed issue order:
+  // each score MFMA of the next half is followed by the exponential work of
+  // one element pair of the current half (fma, exp, exp, cvt, dot2), each
+  // P.V MFMA of the current half by a share of the next half's row max.
+  // Operands from LDS are read two MFMAs ahead; sched_barrier fences keep
+  // the compiler from regrouping the MFMAs and the VALU work.
+  constexpr int NKK = D / 16;                 // score MFMAs per query half
+  constexpr int PPM = 16 / (2 * NKK);         // element pairs per score MFMA
+  constexpr int NPV = 2 * (D / 32);           // (chunk, dim block) pairs
+  auto sub = [&](f32x16 (&cur)[2], f32x16 (&nxt)[2], const uint16_t* ksn, int h2n,
+                 const uint16_t* vs, int c0) __attribute__((always_inline)) {
+    const uint16_t* kr = ksn + (h2n * 32 + ln) * L::KS + hl * 8;
+    const uint16_t* vr = vs + vlane + c0 * 16 * L::VS;
+    float nr[2] = {-mref[0], -mref[1]};
+    uint32_t wds[2][8];
+    // one element pair of the current half: P values, bf16 word, row sum
+    auto pair = [&](int qh, int e) __attribute__((always_inline)) {
+      const float p0 = __builtin_amdgcn_exp2f(fmaf(cur[qh][2 * e], sl2, nr[qh]));
+      const float p1 = __builtin_amdgcn_exp2f(fmaf(cur[qh][2 * e + 1], sl2, nr[qh]));
+      wds[qh][e] = pack_bf16x2(p0, p1);
+      lsum[qh] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, wds[qh][e]), ones,
+                                                 lsum[qh], false);
+    };
+    bf16x8 kf[NKK];
+    kf[0] = *reinterpret_cast<const bf16x8*>(kr);
+    kf[1] = *reinterpret_cast<const bf16x8*>(kr + 16);
+#pragma unroll
+    for (int qh = 0; qh < 2; ++qh)
+#pragma unroll
+      for (int j = 0; j < 16; ++j) nxt[qh][j] = 0.0f;
+#pragma unroll
+    for (int kk = 0; kk < NKK; ++kk) {
+      if (kk + 2 < NKK) kf[kk + 2] = *reinterpret_cast<const bf16x8*>(kr + (kk + 2) * 16);
+#pragma unroll
+      for (int qh = 0; qh < 2; ++qh) {
+        nxt[qh] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[kk], qf[qh][kk], nxt[qh], 0, 0, 0);
+        const int m = kk * 2 + qh;
+#pragma unroll
+        for (int r = 0; r < PPM; ++r) pair((m * PPM + r) / 8, (m * PPM + r) % 8);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+    bf16x8 pb[2][2];
+#pragma unroll
+    for (int qh = 0; qh < 2; ++qh)
+#pragma unroll
+      for (int cc = 0; cc < 2; ++cc) {
+        uint32_t w4[4] = {wds[qh][cc * 4], wds[qh][cc * 4 + 1], wds[qh][cc * 4 + 2], wds[qh][cc * 4 + 3]};
+        pb[qh][cc] = __builtin_bit_cast(bf16x8, w4);
+      }
+    // P.V with V^T operands read two (chunk, dim block) pairs ahead
+    auto vread = [&](int n) __attribute__((always_inline)) {
+      const uint16_t* pp = vr + (n / (D / 32)) * 16 * L::VS + (n % (D / 32)) * 32;
+      const i16x4 r0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+          (__attribute__((address_space(3))) i16x4*)(pp));
+      const i16x4 r1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+          (__attribute__((address_space(3))) i16x4*)(pp + 8 * L::VS));
+      return __builtin_bit_cast(bf16x8, __builtin_shufflevector(r0, r1, 0, 1, 2, 3, 4, 5, 6, 7));
+    };
+    bf16x8 vf[NPV];
+    vf[0] = vread(0);
+    vf[1] = vread(1);
+    float amax[2] = {-INFINITY, -INFINITY};
+    constexpr int MAXPM = 16 / NPV;           // max3 ops per P.V MFMA (second half)
+#pragma unroll
+    for (int n = 0; n < NPV; ++n) {
+      if (n + 2 < NPV) vf[n + 2] = vread(n + 2);
+      const int cc = n / (D / 32), td = n % (D / 32);
+#pragma unroll
+      for (int qh = 0; qh < 2; ++qh) {
+        oacc[qh][td] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[n], pb[qh][cc], oacc[qh][td], 0, 0, 0);
+        if (n >= NPV / 2) {
+          const int q = (n - NPV / 2) * 2 + qh;         // 0 .. NPV-1
+#pragma unroll
+          for (int r = 0; r < MAXPM; ++r) {
+            const int idx2 = (q * MAXPM + r);           // 0 .. 15 over both halves
+            const int hq = idx2 / 8, j = (idx2 % 8) * 2;
+            amax[hq] = fmaxf(amax[hq], fmaxf(nxt[hq][j], nxt[hq][j + 1]));
+          }
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+    float mx[2];
+#pragma unroll
+    for (int qh = 0; qh < 2; ++qh) mx[qh] = max_other_half(amax[qh]) * sl2;
+    apply_ref(mx);
+  };
+  f32x16 sX[2], sY[2];
+  // off-diagonal tile t < nofft-1: both halves, the second computing the
+  // first half of tile t+1
+  auto tile_step = [&](int t) __attribute__((always_inline)) {
+    stage_io(t);
+    const uint16_t* kt = lds + stv * L::STAGE;
+    const uint16_t* vs = kt + L::K_ELEMS;
+    sub(sX, sY, kt, 1, vs, 0);
+    sub(sY, sX, lds + stk * L::STAGE, 0, vs, 2);
+    next_stage();
+  };
+  auto tile_last = [&](int t) __attribute__((always_inline)) {
+    stage_io(t);
+    const uint16_t* kt = lds + stv * L::STAGE;
+    const uint16_t* vs = kt + L::K_ELEMS;
+    sub(sX, sY, kt, 1, vs, 0);
+    bf16x8 pb[2][2];
+    softmax_sub(sY, pb);
+    pv_sub(vs, pb, 2);
+    next_stage();
+  };
+  // diagonal-block tile, not pipelined: scores, mask, max, P, P.V per half
+  auto tile_diag = [&](int t) __attribute__((always_inline)) {
+    stage_io(t);
+    const uint16_t* kt = lds + stv * L::STAGE;
+    const uint16_t* vs = kt + L::K_ELEMS;
+#pragma unroll
+    for (int h2 = 0; h2 < 2; ++h2) {
+      qk_sub(kt, h2, sX);
+      mask_sub(t, h2, sX);
+      update_ref(sX);
+      bf16x8 pb[2][2];
+      softmax_sub(sX, pb);
+      pv_sub(vs, pb, 2 * h2);
+    }
+    next_stage();
   };
 
   if (ntiles > 0) {
@@ -400,22 +512,15 @@ __global__ __launch_bounds__(256, 1) void attn_prefill_bf16_kernel(
     }
     if (ntiles > 2) load_tile(2);
     __syncthreads();
-    f32x16 sA[2][2], sB[2][2];
-    qk_half(lds, I0{}, sA);
-    qk_half(lds, I1{}, sA);
-    if (nofft == 0) mask_tile(0, sA);
-    update_ref(sA);
     int t = 0;
-    for (; t + 2 < ntiles; t += 2) {
-      step(t, sA, sB);
-      step(t + 1, sB, sA);
+    if (nofft > 0) {
+      qk_sub(lds, 0, sX);
+      update_ref(sX);
+      for (; t + 1 < nofft; ++t) tile_step(t);
+      tile_last(t);
+      ++t;
     }
-    if (t + 1 < ntiles) {
-      step(t, sA, sB);
-      last(sB);
-    } else {
-      last(sA);
-    }
+    for (; t < ntiles; ++t) tile_diag(t);
   }
 
   // ---- epilogue ----
