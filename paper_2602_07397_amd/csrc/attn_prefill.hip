@@ -51,6 +51,7 @@ constexpr int KT = 64;                 // keys per LDS tile
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kRescaleSlack = 8.0f;  // log2 units
 constexpr float kNoRef = -1.0e30f;     // exponent reference before any key
+constexpr float kSumLimit = 65536.0f;  // bound on a pipelined P tile's partial row sum
 
 
 // ---------------------------------------------------------------------------
@@ -377,30 +378,106 @@ __global__ __launch_bounds__(256, 1) void attn_prefill_bf16_kernel(
   // Pipeline sub-step over 32 keys: P of the current half and its P.V while
   // the scores of the next half run on the MFMAs; the next half's row max
   // overlaps the P.V MFMAs.
-  // One pipeline sub-step over 32 keys, written as a fixed issue order:
-  // each score MFMA of the next half is followed by the exponential work of
-  // one element pair of the current half (fma, exp, exp, cvt, dot2), each
-  // P.V MFMA of the current half by a share of the next half's row max.
-  // Operands from LDS are read two MFMAs ahead; sched_barrier fences keep
-  // the compiler from regrouping the MFMAs and the VALU work.
+  // One pipeline sub-step over 32 keys, u, written as a fixed issue order.
+  // Phase A: the 16 score MFMAs of sub-step u+1, each pair of them followed
+  // by the exponential work (fma, exp, exp, cvt, dot2) of one element pair of
+  // chunk 1 (keys 16..31) of P(u). Phase B: the 16 P.V MFMAs of sub-step u,
+  // each pair followed by one element pair of chunk 0 (keys 0..15) of
+  // P(u+1). The exponent reference does not follow the row max on this path:
+  // between the phases, a row whose partial sum over P(u) exceeds
+  // 2^kSumLimit (which bounds every element of it) moves its reference to
+  // the exact row max of the sub-step, rescales O and its sum and recomputes
+  // P(u) (rare: a wave-uniform branch). Operands from LDS are read two MFMAs
+  // ahead; sched_barrier fences keep the compiler from regrouping the MFMAs
+  // and the VALU work.
   constexpr int NKK = D / 16;                 // score MFMAs per query half
-  constexpr int PPM = 16 / (2 * NKK);         // element pairs per score MFMA
   constexpr int NPV = 2 * (D / 32);           // (chunk, dim block) pairs
-  auto sub = [&](f32x16 (&cur)[2], f32x16 (&nxt)[2], const uint16_t* ksn, int h2n,
+  constexpr int QK_PER_PAIR = (2 * NKK) / 8;  // score MFMAs per element pair
+  constexpr int PV_PER_PAIR = (2 * NPV) / 8;  // P.V MFMAs per element pair
+  // element pair e (elements 2e, 2e+1) of S[qh]: P word and partial row sum
+  auto pair = [&](f32x16 (&S)[2], int qh, int e, uint32_t& word, float& ts)
+      __attribute__((always_inline)) {
+    const float nr = -mref[qh];
+    const float p0 = __builtin_amdgcn_exp2f(fmaf(S[qh][2 * e], sl2, nr));
+    const float p1 = __builtin_amdgcn_exp2f(fmaf(S[qh][2 * e + 1], sl2, nr));
+    word = pack_bf16x2(p0, p1);
+    ts = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, word), ones, ts, false);
+  };
+  auto vread = [&](const uint16_t* vr, int n) __attribute__((always_inline)) {
+    const uint16_t* pp = vr + (n / (D / 32)) * 16 * L::VS + (n % (D / 32)) * 32;
+    const i16x4 r0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (__attribute__((address_space(3))) i16x4*)(pp));
+    const i16x4 r1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (__attribute__((address_space(3))) i16x4*)(pp + 8 * L::VS));
+    return __builtin_bit_cast(bf16x8, __builtin_shufflevector(r0, r1, 0, 1, 2, 3, 4, 5, 6, 7));
+  };
+  // rare path: exact row max of S, new reference, rescale, recompute P(u)
+  auto refix = [&](f32x16 (&S)[2], uint32_t (&w0)[2][4], uint32_t (&w1)[2][4], float (&ts)[2])
+      __attribute__((always_inline)) {
+    float mx[2];
+    row_max(S, mx);
+#pragma unroll
+    for (int qh = 0; qh < 2; ++qh) {
+      const float nref = fmaxf(mref[qh], mx[qh]);
+      const float alpha = __builtin_amdgcn_exp2f(mref[qh] - nref);
+      mref[qh] = nref;
+      lsum[qh] *= alpha;
+#pragma unroll
+      for (int td = 0; td < D / 32; ++td)
+#pragma unroll
+        for (int j = 0; j < 16; ++j) oacc[qh][td][j] *= alpha;
+      ts[qh] = 0.0f;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) pair(S, qh, e, w0[qh][e], ts[qh]);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) pair(S, qh, 4 + e, w1[qh][e], ts[qh]);
+    }
+  };
+  // check of P(u) between the phases; adds its sums
+  auto check = [&](f32x16 (&cur)[2], uint32_t (&w0)[2][4], uint32_t (&w1)[2][4], float (&ts)[2])
+      __attribute__((always_inline)) {
+    if (__any(ts[0] > kSumLimit || ts[1] > kSumLimit)) refix(cur, w0, w1, ts);
+    lsum[0] += ts[0];
+    lsum[1] += ts[1];
+  };
+  // phase B: P.V of sub-step u (words w0: chunk 0, w1: chunk 1), with the
+  // chunk-0 exponentials of the next sub-step's scores when HAS_NEXT
+  auto phase_b = [&](const uint16_t* vr, uint32_t (&w0)[2][4], uint32_t (&w1)[2][4],
+                     bf16x8 (&vf)[NPV], f32x16 (&nxt)[2], uint32_t (&wn)[2][4], float (&tn)[2],
+                     auto has_next) __attribute__((always_inline)) {
+    constexpr bool HAS_NEXT = decltype(has_next)::value;
+    bf16x8 pb[2][2];
+#pragma unroll
+    for (int qh = 0; qh < 2; ++qh) {
+      pb[qh][0] = __builtin_bit_cast(bf16x8, w0[qh]);
+      pb[qh][1] = __builtin_bit_cast(bf16x8, w1[qh]);
+    }
+    tn[0] = 0.0f;
+    tn[1] = 0.0f;
+#pragma unroll
+    for (int n = 0; n < NPV; ++n) {
+      if (n + 2 < NPV) vf[n + 2] = vread(vr, n + 2);
+      const int cc = n / (D / 32), td = n % (D / 32);
+#pragma unroll
+      for (int qh = 0; qh < 2; ++qh) {
+        oacc[qh][td] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[n], pb[qh][cc], oacc[qh][td], 0, 0, 0);
+        const int m = n * 2 + qh;
+        if (HAS_NEXT && (m % PV_PER_PAIR) == PV_PER_PAIR - 1) {
+          const int pr = m / PV_PER_PAIR;              // 0..7
+          pair(nxt, pr / 4, pr % 4, wn[pr / 4][pr % 4], tn[pr / 4]);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+  };
+  auto sub = [&](f32x16 (&cur)[2], uint32_t (&wc)[2][4], float (&tc)[2], f32x16 (&nxt)[2],
+                 uint32_t (&wn)[2][4], float (&tn)[2], const uint16_t* ksn, int h2n,
                  const uint16_t* vs, int c0) __attribute__((always_inline)) {
     const uint16_t* kr = ksn + (h2n * 32 + ln) * L::KS + hl * 8;
     const uint16_t* vr = vs + vlane + c0 * 16 * L::VS;
-    float nr[2] = {-mref[0], -mref[1]};
-    uint32_t wds[2][8];
-    // one element pair of the current half: P values, bf16 word, row sum
-    auto pair = [&](int qh, int e) __attribute__((always_inline)) {
-      const float p0 = __builtin_amdgcn_exp2f(fmaf(cur[qh][2 * e], sl2, nr[qh]));
-      const float p1 = __builtin_amdgcn_exp2f(fmaf(cur[qh][2 * e + 1], sl2, nr[qh]));
-      wds[qh][e] = pack_bf16x2(p0, p1);
-      lsum[qh] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, wds[qh][e]), ones,
-                                                 lsum[qh], false);
-    };
+    uint32_t w1[2][4];
     bf16x8 kf[NKK];
+    bf16x8 vf[NPV];
     kf[0] = *reinterpret_cast<const bf16x8*>(kr);
     kf[1] = *reinterpret_cast<const bf16x8*>(kr + 16);
 #pragma unroll
@@ -410,80 +487,55 @@ __global__ __launch_bounds__(256, 1) void attn_prefill_bf16_kernel(
 #pragma unroll
     for (int kk = 0; kk < NKK; ++kk) {
       if (kk + 2 < NKK) kf[kk + 2] = *reinterpret_cast<const bf16x8*>(kr + (kk + 2) * 16);
+      if (kk == NKK - 2) vf[0] = vread(vr, 0);
+      if (kk == NKK - 1) vf[1] = vread(vr, 1);
 #pragma unroll
       for (int qh = 0; qh < 2; ++qh) {
         nxt[qh] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[kk], qf[qh][kk], nxt[qh], 0, 0, 0);
         const int m = kk * 2 + qh;
-#pragma unroll
-        for (int r = 0; r < PPM; ++r) pair((m * PPM + r) / 8, (m * PPM + r) % 8);
-        __builtin_amdgcn_sched_barrier(0);
-      }
-    }
-    bf16x8 pb[2][2];
-#pragma unroll
-    for (int qh = 0; qh < 2; ++qh)
-#pragma unroll
-      for (int cc = 0; cc < 2; ++cc) {
-        uint32_t w4[4] = {wds[qh][cc * 4], wds[qh][cc * 4 + 1], wds[qh][cc * 4 + 2], wds[qh][cc * 4 + 3]};
-        pb[qh][cc] = __builtin_bit_cast(bf16x8, w4);
-      }
-    // P.V with V^T operands read two (chunk, dim block) pairs ahead
-    auto vread = [&](int n) __attribute__((always_inline)) {
-      const uint16_t* pp = vr + (n / (D / 32)) * 16 * L::VS + (n % (D / 32)) * 32;
-      const i16x4 r0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-          (__attribute__((address_space(3))) i16x4*)(pp));
-      const i16x4 r1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-          (__attribute__((address_space(3))) i16x4*)(pp + 8 * L::VS));
-      return __builtin_bit_cast(bf16x8, __builtin_shufflevector(r0, r1, 0, 1, 2, 3, 4, 5, 6, 7));
-    };
-    bf16x8 vf[NPV];
-    vf[0] = vread(0);
-    vf[1] = vread(1);
-    float amax[2] = {-INFINITY, -INFINITY};
-    constexpr int MAXPM = 16 / NPV;           // max3 ops per P.V MFMA (second half)
-#pragma unroll
-    for (int n = 0; n < NPV; ++n) {
-      if (n + 2 < NPV) vf[n + 2] = vread(n + 2);
-      const int cc = n / (D / 32), td = n % (D / 32);
-#pragma unroll
-      for (int qh = 0; qh < 2; ++qh) {
-        oacc[qh][td] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[n], pb[qh][cc], oacc[qh][td], 0, 0, 0);
-        if (n >= NPV / 2) {
-          const int q = (n - NPV / 2) * 2 + qh;         // 0 .. NPV-1
-#pragma unroll
-          for (int r = 0; r < MAXPM; ++r) {
-            const int idx2 = (q * MAXPM + r);           // 0 .. 15 over both halves
-            const int hq = idx2 / 8, j = (idx2 % 8) * 2;
-            amax[hq] = fmaxf(amax[hq], fmaxf(nxt[hq][j], nxt[hq][j + 1]));
-          }
+        if ((m % QK_PER_PAIR) == QK_PER_PAIR - 1) {
+          const int pr = m / QK_PER_PAIR;              // 0..7
+          pair(cur, pr / 4, 4 + pr % 4, w1[pr / 4][pr % 4], tc[pr / 4]);
         }
         __builtin_amdgcn_sched_barrier(0);
       }
     }
-    float mx[2];
+    check(cur, wc, w1, tc);
+    phase_b(vr, wc, w1, vf, nxt, wn, tn, std::true_type{});
+  };
+  // final sub-step of the off-diagonal run: no scores ahead
+  auto sub_last = [&](f32x16 (&cur)[2], uint32_t (&wc)[2][4], float (&tc)[2],
+                      const uint16_t* vs, int c0) __attribute__((always_inline)) {
+    const uint16_t* vr = vs + vlane + c0 * 16 * L::VS;
+    uint32_t w1[2][4];
+    bf16x8 vf[NPV];
+    vf[0] = vread(vr, 0);
+    vf[1] = vread(vr, 1);
 #pragma unroll
-    for (int qh = 0; qh < 2; ++qh) mx[qh] = max_other_half(amax[qh]) * sl2;
-    apply_ref(mx);
+    for (int pr = 0; pr < 8; ++pr) pair(cur, pr / 4, 4 + pr % 4, w1[pr / 4][pr % 4], tc[pr / 4]);
+    check(cur, wc, w1, tc);
+    float tdummy[2];
+    phase_b(vr, wc, w1, vf, cur, wc, tdummy, std::false_type{});
   };
   f32x16 sX[2], sY[2];
+  uint32_t wX[2][4], wY[2][4];
+  float tX[2], tY[2];
   // off-diagonal tile t < nofft-1: both halves, the second computing the
   // first half of tile t+1
   auto tile_step = [&](int t) __attribute__((always_inline)) {
     stage_io(t);
     const uint16_t* kt = lds + stv * L::STAGE;
     const uint16_t* vs = kt + L::K_ELEMS;
-    sub(sX, sY, kt, 1, vs, 0);
-    sub(sY, sX, lds + stk * L::STAGE, 0, vs, 2);
+    sub(sX, wX, tX, sY, wY, tY, kt, 1, vs, 0);
+    sub(sY, wY, tY, sX, wX, tX, lds + stk * L::STAGE, 0, vs, 2);
     next_stage();
   };
   auto tile_last = [&](int t) __attribute__((always_inline)) {
     stage_io(t);
     const uint16_t* kt = lds + stv * L::STAGE;
     const uint16_t* vs = kt + L::K_ELEMS;
-    sub(sX, sY, kt, 1, vs, 0);
-    bf16x8 pb[2][2];
-    softmax_sub(sY, pb);
-    pv_sub(vs, pb, 2);
+    sub(sX, wX, tX, sY, wY, tY, kt, 1, vs, 0);
+    sub_last(sY, wY, tY, vs, 2);
     next_stage();
   };
   // diagonal-block tile, not pipelined: scores, mask, max, P, P.V per half
@@ -514,8 +566,15 @@ __global__ __launch_bounds__(256, 1) void attn_prefill_bf16_kernel(
     __syncthreads();
     int t = 0;
     if (nofft > 0) {
+      // scores of the first half tile; its chunk-0 words are left to the
+      // first check (an infinite partial sum forces the exact reference)
       qk_sub(lds, 0, sX);
-      update_ref(sX);
+#pragma unroll
+      for (int qh = 0; qh < 2; ++qh) {
+        tX[qh] = INFINITY;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) wX[qh][e] = 0u;
+      }
       for (; t + 1 < nofft; ++t) tile_step(t);
       tile_last(t);
       ++t;
