@@ -4,36 +4,41 @@
 // over those keys only.
 //
 // bf16 kernel. Work item = (query block, KV head g, slice of the group's query
-// heads). A 256-thread workgroup has 4 wavefronts; each owns 64 query rows
-// (one head; a B = 128 block takes two wavefronts per head, a B = 64 block
-// one), so a workgroup serves two (B = 128) or four (B = 64) query heads of
-// the same KV group from one copy of each K/V tile in LDS. One wavefront per
-// SIMD with the full 512-entry register file: the 64-row tile halves the LDS
-// bytes read per MFMA compared with 32-row wavefronts.
+// heads). A 512-thread workgroup has 8 wavefronts, two per SIMD; each owns 32
+// query rows of one head (a B = 128 block takes four wavefronts per head, a
+// B = 64 block two), so a workgroup serves two (B = 128) or four (B = 64)
+// query heads of the same KV group from one copy of each K/V tile in LDS.
+// The two wavefronts of a SIMD cover each other's LDS and barrier waits.
 //
-// Per wavefront and 64-key tile the scores are computed transposed,
+// Per wavefront and 32-key sub-tile the scores are computed transposed,
 // S^T = K Q^T (v_mfma_f32_32x32x16_bf16, fp32 accumulate), so a lane owns one
-// query column: its running max and sum stay in the lane plus one
-// v_permlane32_swap with the other half-wave. P (rounded to bf16) feeds the B
-// operand of O^T = V^T P^T straight from the accumulator layout. V stays in
+// query column and its partial row sum; the other half-wave holds the rest of
+// the row (one v_permlane32_swap combines them). P (rounded to bf16) feeds the
+// B operand of O^T = V^T P^T straight from the accumulator layout. V stays in
 // its natural row layout in LDS and the V^T operand is read with
 // ds_read_b64_tr_b16, which hands each lane four consecutive keys of one
 // dimension.
 //
-// Software pipeline over tiles: while the exponentials of tile t run on the
-// VALU, the MFMAs compute the scores of tile t+1; the row max of t+1 is taken
-// during the P.V MFMAs of tile t. K/V tiles go through three LDS stages from
-// registers loaded one tile ahead. The exponent reference of a row moves only
-// when its max grows by more than kRescaleSlack (log2 units), so the O
-// rescale is rare; P then stays below 2^kRescaleSlack.
+// Software pipeline over 32-key sub-tiles u, in a fixed issue order:
+//   phase A: the score MFMAs of u+1, interleaved with the exponentials of
+//            keys 16..31 of P(u);
+//   phase B: the P.V MFMAs of u, interleaved with the exponentials of keys
+//            0..15 of P(u+1).
+// The exponent reference of a row does not track the row max on this path:
+// between the phases, a row whose partial sum over P(u) exceeds kSumLimit
+// (which bounds every element) takes the exact max of the sub-tile, rescales
+// O and its sum and recomputes P(u) (rare, wave-uniform branch). Since
+// O = sum(P V) / sum(P) for any common reference, the result does not depend
+// on which reference was used.
 //
-// The selected blocks are compacted in LDS at the start: valid blocks j < i
-// first (never masked: only a sequence's last block can be partial), then the
-// diagonal block i, whose tiles apply the causal and sequence-end masks.
-// Work items run longest-first (query blocks in descending order, the
-// selection budget grows with the block index) and the workgroups of one
-// (query block, KV head) are placed on one XCD so they share the K/V blocks
-// through that XCD's L2.
+// K/V tiles of 64 keys go through three LDS stages from registers loaded one
+// tile ahead. The selected blocks are compacted in LDS at the start: valid
+// blocks j < i first (never masked: only a sequence's last block can be
+// partial), then the diagonal block i, whose tiles are processed without the
+// pipeline and with the causal and sequence-end masks. Work items run
+// longest-first (query blocks in descending order, the selection budget grows
+// with the block index) and the workgroups of one (query block, KV head) are
+// placed on one XCD so they share the K/V blocks through that XCD's L2.
 #include <type_traits>
 
 #include "sw_common.h"
@@ -44,15 +49,14 @@ namespace sw {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
-typedef short i16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 constexpr int KT = 64;                 // keys per LDS tile
 constexpr float kLog2e = 1.4426950408889634f;
-constexpr float kRescaleSlack = 8.0f;  // log2 units
+constexpr float kRescaleSlack = 8.0f;  // log2 units (diagonal tiles)
 constexpr float kNoRef = -1.0e30f;     // exponent reference before any key
-constexpr float kSumLimit = 65536.0f;  // bound on a pipelined P tile's partial row sum
-
+constexpr float kSumLimit = 65536.0f;  // bound on a pipelined P sub-tile's partial row sum
+constexpr int kPfWaves = 8;            // wavefronts per bf16 workgroup
 
 // ---------------------------------------------------------------------------
 // work mapping
@@ -114,16 +118,19 @@ __device__ __forceinline__ float sum_other_half(float v) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
+#define SW_INL __attribute__((always_inline))
+
 template <int D, int BLK>
-__global__ __launch_bounds__(256, 1) void attn_prefill_bf16_kernel(
+__global__ __launch_bounds__(kPfWaves * 64, 1) void attn_prefill_bf16_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
     const uint16_t* __restrict__ V, int h_q, int h_kv, long long N, SeqMeta m,
     const int32_t* __restrict__ idx, const int32_t* __restrict__ cnt, int kmax, float sl2,
     uint16_t* __restrict__ O, float* __restrict__ lse, int groups, int sg) {
   using L = BfLds<D>;
+  constexpr int NT = kPfWaves * 64;        // threads
   __shared__ __attribute__((aligned(16))) uint16_t lds[L::NST * L::STAGE];
   __shared__ int blist[SW_MAX_BLOCKS];
-  __shared__ int wtot[4];
+  __shared__ int wtot[kPfWaves];
   __shared__ int sdiag;
 
   // ---- work item ----
@@ -137,7 +144,7 @@ __global__ __launch_bounds__(256, 1) void attn_prefill_bf16_kernel(
   const int g = gamma % h_kv;
   int row, s, i;
   lpt_row(m, rho, &row, &s, &i);
-  constexpr int WPB = BLK / 64;            // wavefronts per (query head, block)
+  constexpr int WPB = BLK / 32;            // wavefronts per (query head, block)
   constexpr int TPB = BLK / KT;            // key tiles per block
   const int G = h_q / h_kv;
   const int tid = threadIdx.x;
@@ -145,24 +152,23 @@ __global__ __launch_bounds__(256, 1) void attn_prefill_bf16_kernel(
   const int l = tid & 63;
   const int hl = l >> 5;                   // half-wave
   const int ln = l & 31;                   // lane within half
-  const int task = mu * 4 + w;
+  const int task = mu * kPfWaves + w;
   const int u = g * G + task / WPB;        // query head (meaningful only when active)
   const int seq0 = m.tok_start[s];
   const int seq1 = m.tok_start[s + 1];
-  const int q0 = seq0 + i * BLK + (task % WPB) * 64;   // first query row of this wavefront
+  const int q0 = seq0 + i * BLK + (task % WPB) * 32;   // first query row of this wavefront
   const bool active = (task < G * WPB) && (q0 < seq1);
+  const int qpos = q0 + ln;                // this lane's query row
 
-  // ---- Q fragments: lane holds query q0 + qh*32 + ln, dims kk*16 + hl*8 .. +7 ----
-  bf16x8 qf[2][D / 16];
-#pragma unroll
-  for (int qh = 0; qh < 2; ++qh) {
-    const int qp = q0 + qh * 32 + ln;
-    const bool ok = active && qp < seq1;
-    const uint16_t* qrow = Q + ((long long)(ok ? u : 0) * N + (ok ? qp : 0)) * D;
+  // ---- Q fragments: lane holds query qpos, dims kk*16 + hl*8 .. +7 ----
+  bf16x8 qf[D / 16];
+  {
+    const bool ok = active && qpos < seq1;
+    const uint16_t* qrow = Q + ((long long)(ok ? u : 0) * N + (ok ? qpos : 0)) * D;
 #pragma unroll
     for (int kk = 0; kk < D / 16; ++kk) {
       uint4 v = ok ? *reinterpret_cast<const uint4*>(qrow + kk * 16 + hl * 8) : make_uint4(0, 0, 0, 0);
-      qf[qh][kk] = *reinterpret_cast<bf16x8*>(&v);
+      qf[kk] = __builtin_bit_cast(bf16x8, v);
     }
   }
 
@@ -172,7 +178,7 @@ __global__ __launch_bounds__(256, 1) void attn_prefill_bf16_kernel(
   if (tid == 0) sdiag = 0;
   __syncthreads();
   int n_off = 0;
-  for (int base = 0; base < nsel; base += 256) {
+  for (int base = 0; base < nsel; base += NT) {
     const int e = base + tid;
     const int j = (e < nsel) ? sel[e] : -1;
     const bool off = (j >= 0 && j < i);
@@ -183,7 +189,7 @@ __global__ __launch_bounds__(256, 1) void attn_prefill_bf16_kernel(
     __syncthreads();
     int woff = 0, tot = 0;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
+    for (int q = 0; q < kPfWaves; ++q) {
       woff += (q < w) ? wtot[q] : 0;
       tot += wtot[q];
     }
@@ -198,12 +204,13 @@ __global__ __launch_bounds__(256, 1) void attn_prefill_bf16_kernel(
 
   // ---- K/V staging: global -> registers -> LDS, 16-byte chunks ----
   constexpr int KCH = D / 8;               // chunks per key row
-  constexpr int KP = (KT * KCH) / 256;     // chunks per thread for K (and for V)
+  constexpr int KP = (KT * KCH) / NT;      // chunks per thread for K (and for V)
+  static_assert(KP >= 1 && KP * NT == KT * KCH, "tile chunks must divide over the workgroup");
   uint4 kreg[KP], vreg[KP];
   int goff[KP], kloff[KP], vloff[KP];
 #pragma unroll
   for (int p = 0; p < KP; ++p) {
-    const int e = tid + p * 256;
+    const int e = tid + p * NT;
     const int r = e / KCH, ch = e % KCH;
     goff[p] = (r * D + ch * 8) * 2;
     kloff[p] = r * L::KS + ch * 8;
@@ -211,7 +218,7 @@ __global__ __launch_bounds__(256, 1) void attn_prefill_bf16_kernel(
   }
   const uint16_t* Kg = K + (long long)g * N * D;
   const uint16_t* Vg = V + (long long)g * N * D;
-  auto tile_k0 = [&](int t) __attribute__((always_inline)) {
+  auto tile_k0 = [&](int t) SW_INL {
     const int jj = t / TPB;
     const int j = (jj < n_off) ? blist[jj] : i;
     return seq0 + j * BLK + (t % TPB) * KT;
@@ -219,7 +226,7 @@ __global__ __launch_bounds__(256, 1) void attn_prefill_bf16_kernel(
   // Raw buffer loads through a descriptor based at the tile's first key and
   // sized to the end of the sequence: keys past the end read as zero without
   // per-lane tests (the diagonal-tile mask removes them).
-  auto load_tile = [&](int t) __attribute__((always_inline)) {
+  auto load_tile = [&](int t) SW_INL {
     const int k0 = tile_k0(t);
     const int bytes = max(0, (seq1 - k0) * D * 2);
     const __amdgpu_buffer_rsrc_t rk =
@@ -229,12 +236,12 @@ __global__ __launch_bounds__(256, 1) void attn_prefill_bf16_kernel(
 #pragma unroll
     for (int p = 0; p < KP; ++p) {
       auto a = __builtin_amdgcn_raw_buffer_load_b128(rk, goff[p], 0, 0);
-      kreg[p] = *reinterpret_cast<uint4*>(&a);
+      kreg[p] = __builtin_bit_cast(uint4, a);
       auto b = __builtin_amdgcn_raw_buffer_load_b128(rv, goff[p], 0, 0);
-      vreg[p] = *reinterpret_cast<uint4*>(&b);
+      vreg[p] = __builtin_bit_cast(uint4, b);
     }
   };
-  auto store_tile = [&](int st) __attribute__((always_inline)) {
+  auto store_tile = [&](int st) SW_INL {
     uint16_t* ks = lds + st * L::STAGE;
     uint16_t* vs = ks + L::K_ELEMS;
 #pragma unroll
@@ -245,165 +252,70 @@ __global__ __launch_bounds__(256, 1) void attn_prefill_bf16_kernel(
   };
 
   // ---- running state ----
-  f32x16 oacc[2][D / 32];
+  f32x16 oacc[D / 32];
 #pragma unroll
-  for (int qh = 0; qh < 2; ++qh)
+  for (int td = 0; td < D / 32; ++td)
+#pragma unroll
+    for (int j = 0; j < 16; ++j) oacc[td][j] = 0.0f;
+  float mref = kNoRef;
+  float lsum = 0.0f;
+  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+  constexpr int NKK = D / 16;              // score MFMAs per sub-tile
+  constexpr int NPV = 2 * (D / 32);        // P.V MFMAs per sub-tile: (chunk, dim block)
+  constexpr int QK_PER_PAIR = NKK / 4;     // score MFMAs per element pair (phase A)
+  constexpr int PV_PER_PAIR = NPV / 4;     // P.V MFMAs per element pair (phase B)
+  // V^T operand lane offset: lane (ln, hl) reads with ds_read_b64_tr_b16 from
+  // key row c*16 + 4*hl + (ln%16)/4 (+8) and dims td*32 + 16*(ln/16) + 4*(ln%4);
+  // it receives dim td*32 + ln of keys c*16 + 4*hl + 0..3 and
+  // c*16 + 8 + 4*hl + 0..3, the keys its P operand holds.
+  const int vlane = (4 * hl + ((ln & 15) >> 2)) * L::VS + 16 * (ln >> 4) + 4 * (ln & 3);
+
+  // Scores of 32 keys (half h2 of a 64-key tile) x 32 queries, transposed:
+  // element j is key h2*32 + 8*(j/4) + 4*hl + j%4, query qpos.
+  auto qk_sub = [&](const uint16_t* ks, int h2, f32x16& S) SW_INL {
+#pragma unroll
+    for (int j = 0; j < 16; ++j) S[j] = 0.0f;
+    const uint16_t* kr = ks + (h2 * 32 + ln) * L::KS + hl * 8;
+#pragma unroll
+    for (int kk = 0; kk < NKK; ++kk) {
+      const bf16x8 a = *reinterpret_cast<const bf16x8*>(kr + kk * 16);
+      S = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[kk], S, 0, 0, 0);
+    }
+  };
+  // causal + sequence-end mask of a diagonal-block sub-tile (raw scores)
+  auto mask_sub = [&](int t, int h2, f32x16& S) SW_INL {
+    const int k0 = tile_k0(t) + h2 * 32;
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      const int kp = k0 + (j >> 2) * 8 + hl * 4 + (j & 3);
+      if (kp > qpos || kp >= seq1) S[j] = -INFINITY;
+    }
+  };
+  // row max of a sub-tile (log2 units)
+  auto row_max = [&](const f32x16& S) SW_INL {
+    float a = -INFINITY;
+#pragma unroll
+    for (int j = 0; j < 16; ++j) a = fmaxf(a, S[j]);
+    return max_other_half(a) * sl2;
+  };
+  auto rescale_to = [&](float nref) SW_INL {
+    const float alpha = __builtin_amdgcn_exp2f(mref - nref);
+    mref = nref;
+    lsum *= alpha;
 #pragma unroll
     for (int td = 0; td < D / 32; ++td)
 #pragma unroll
-      for (int j = 0; j < 16; ++j) oacc[qh][td][j] = 0.0f;
-  float mref[2] = {kNoRef, kNoRef};
-  float lsum[2] = {0.0f, 0.0f};
-  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
-
-  // Scores of 32 keys (half h2 of a 64-key tile) x 64 queries, transposed:
-  // S[qh] element j is key h2*32 + 8*(j/4) + 4*hl + j%4, query qh*32 + ln.
-  auto qk_sub = [&](const uint16_t* ks, int h2, f32x16 (&S)[2]) __attribute__((always_inline)) {
-#pragma unroll
-    for (int qh = 0; qh < 2; ++qh)
-#pragma unroll
-      for (int j = 0; j < 16; ++j) S[qh][j] = 0.0f;
-    const uint16_t* kr = ks + (h2 * 32 + ln) * L::KS + hl * 8;
-#pragma unroll
-    for (int kk = 0; kk < D / 16; ++kk) {
-      const bf16x8 a = *reinterpret_cast<const bf16x8*>(kr + kk * 16);
-      S[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[0][kk], S[0], 0, 0, 0);
-      S[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[1][kk], S[1], 0, 0, 0);
-    }
+      for (int j = 0; j < 16; ++j) oacc[td][j] *= alpha;
   };
-  // causal + sequence-end mask of a diagonal-block half tile (raw scores)
-  auto mask_sub = [&](int t, int h2, f32x16 (&S)[2]) __attribute__((always_inline)) {
-    const int k0 = tile_k0(t) + h2 * 32;
-#pragma unroll
-    for (int qh = 0; qh < 2; ++qh) {
-      const int qpos = q0 + qh * 32 + ln;
-#pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        const int kp = k0 + (j >> 2) * 8 + hl * 4 + (j & 3);
-        if (kp > qpos || kp >= seq1) S[qh][j] = -INFINITY;
-      }
-    }
-  };
-  // row max (log2 units)
-  auto row_max = [&](f32x16 (&S)[2], float (&mx)[2]) __attribute__((always_inline)) {
-#pragma unroll
-    for (int qh = 0; qh < 2; ++qh) {
-      float a = -INFINITY;
-#pragma unroll
-      for (int j = 0; j < 16; ++j) a = fmaxf(a, S[qh][j]);
-      mx[qh] = max_other_half(a) * sl2;
-    }
-  };
-  // moves the exponent reference of rows whose max grew by more than the
-  // slack, rescaling O and the sums (rare: a wave-uniform branch)
-  auto apply_ref = [&](const float (&mx)[2]) __attribute__((always_inline)) {
-    const bool n0 = mx[0] > mref[0] + kRescaleSlack;
-    const bool n1 = mx[1] > mref[1] + kRescaleSlack;
-    if (__any(n0 || n1)) {
-#pragma unroll
-      for (int qh = 0; qh < 2; ++qh) {
-        const float nref = (qh ? n1 : n0) ? mx[qh] : mref[qh];
-        const float alpha = __builtin_amdgcn_exp2f(mref[qh] - nref);
-        mref[qh] = nref;
-        lsum[qh] *= alpha;
-#pragma unroll
-        for (int td = 0; td < D / 32; ++td)
-#pragma unroll
-          for (int j = 0; j < 16; ++j) oacc[qh][td][j] *= alpha;
-      }
-    }
-  };
-  auto update_ref = [&](f32x16 (&S)[2]) __attribute__((always_inline)) {
-    float mx[2];
-    row_max(S, mx);
-    apply_ref(mx);
-  };
-  // P = exp2(S*sl2 - ref) for 32 keys (two 16-key chunks), rounded to bf16;
-  // the row sums accumulate the rounded values
-  auto softmax_sub = [&](f32x16 (&S)[2], bf16x8 (&pb)[2][2]) __attribute__((always_inline)) {
-#pragma unroll
-    for (int qh = 0; qh < 2; ++qh) {
-      const float nr = -mref[qh];
-#pragma unroll
-      for (int cc = 0; cc < 2; ++cc) {
-        uint32_t wds[4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const float p0 = __builtin_amdgcn_exp2f(fmaf(S[qh][cc * 8 + 2 * e], sl2, nr));
-          const float p1 = __builtin_amdgcn_exp2f(fmaf(S[qh][cc * 8 + 2 * e + 1], sl2, nr));
-          wds[e] = pack_bf16x2(p0, p1);
-          lsum[qh] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, wds[e]), ones, lsum[qh], false);
-        }
-        pb[qh][cc] = __builtin_bit_cast(bf16x8, wds);
-      }
-    }
-  };
-  // O^T += V^T P^T for the 16-key chunks c0, c0+1 of a tile. Lane (ln, hl)
-  // reads with ds_read_b64_tr_b16 from key row c*16 + 4*hl + (ln%16)/4 (+8)
-  // and dims td*32 + 16*(ln/16) + 4*(ln%4): it receives dim td*32 + ln of keys
-  // c*16 + 4*hl + 0..3 and c*16 + 8 + 4*hl + 0..3, the keys its P operand holds.
-  const int vlane = (4 * hl + ((ln & 15) >> 2)) * L::VS + 16 * (ln >> 4) + 4 * (ln & 3);
-  auto pv_sub = [&](const uint16_t* vs, const bf16x8 (&pb)[2][2], int c0) __attribute__((always_inline)) {
-#pragma unroll
-    for (int cc = 0; cc < 2; ++cc)
-#pragma unroll
-      for (int td = 0; td < D / 32; ++td) {
-        const uint16_t* p = vs + vlane + (c0 + cc) * 16 * L::VS + td * 32;
-        const i16x4 r0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            (__attribute__((address_space(3))) i16x4*)(p));
-        const i16x4 r1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            (__attribute__((address_space(3))) i16x4*)(p + 8 * L::VS));
-        const i16x8 rr = __builtin_shufflevector(r0, r1, 0, 1, 2, 3, 4, 5, 6, 7);
-        const bf16x8 av = __builtin_bit_cast(bf16x8, rr);
-        oacc[0][td] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pb[0][cc], oacc[0][td], 0, 0, 0);
-        oacc[1][td] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pb[1][cc], oacc[1][td], 0, 0, 0);
-      }
-  };
-
-  // Stages: during tile step t, K/V(t) are in stv, K(t+1) in stk, and tile
-  // t+2 is written to stw from the registers loaded during step t-1; tile
-  // t+3 is loaded into those registers.
-  int stv = 0, stk = 1, stw = 2;
-  auto stage_io = [&](int t) __attribute__((always_inline)) {
-    if (t + 2 < ntiles) store_tile(stw);
-    if (t + 3 < ntiles) load_tile(t + 3);
-  };
-  auto next_stage = [&]() __attribute__((always_inline)) {
-    const int t0 = stv;
-    stv = stk;
-    stk = stw;
-    stw = t0;
-    __syncthreads();
-  };
-  // Pipeline sub-step over 32 keys: P of the current half and its P.V while
-  // the scores of the next half run on the MFMAs; the next half's row max
-  // overlaps the P.V MFMAs.
-  // One pipeline sub-step over 32 keys, u, written as a fixed issue order.
-  // Phase A: the 16 score MFMAs of sub-step u+1, each pair of them followed
-  // by the exponential work (fma, exp, exp, cvt, dot2) of one element pair of
-  // chunk 1 (keys 16..31) of P(u). Phase B: the 16 P.V MFMAs of sub-step u,
-  // each pair followed by one element pair of chunk 0 (keys 0..15) of
-  // P(u+1). The exponent reference does not follow the row max on this path:
-  // between the phases, a row whose partial sum over P(u) exceeds
-  // 2^kSumLimit (which bounds every element of it) moves its reference to
-  // the exact row max of the sub-step, rescales O and its sum and recomputes
-  // P(u) (rare: a wave-uniform branch). Operands from LDS are read two MFMAs
-  // ahead; sched_barrier fences keep the compiler from regrouping the MFMAs
-  // and the VALU work.
-  constexpr int NKK = D / 16;                 // score MFMAs per query half
-  constexpr int NPV = 2 * (D / 32);           // (chunk, dim block) pairs
-  constexpr int QK_PER_PAIR = (2 * NKK) / 8;  // score MFMAs per element pair
-  constexpr int PV_PER_PAIR = (2 * NPV) / 8;  // P.V MFMAs per element pair
-  // element pair e (elements 2e, 2e+1) of S[qh]: P word and partial row sum
-  auto pair = [&](f32x16 (&S)[2], int qh, int e, uint32_t& word, float& ts)
-      __attribute__((always_inline)) {
-    const float nr = -mref[qh];
-    const float p0 = __builtin_amdgcn_exp2f(fmaf(S[qh][2 * e], sl2, nr));
-    const float p1 = __builtin_amdgcn_exp2f(fmaf(S[qh][2 * e + 1], sl2, nr));
+  // element pair e (elements 2e, 2e+1): P word and partial row sum
+  auto pair = [&](const f32x16& S, int e, uint32_t& word, float& ts) SW_INL {
+    const float nr = -mref;
+    const float p0 = __builtin_amdgcn_exp2f(fmaf(S[2 * e], sl2, nr));
+    const float p1 = __builtin_amdgcn_exp2f(fmaf(S[2 * e + 1], sl2, nr));
     word = pack_bf16x2(p0, p1);
     ts = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, word), ones, ts, false);
   };
-  auto vread = [&](const uint16_t* vr, int n) __attribute__((always_inline)) {
+  auto vread = [&](const uint16_t* vr, int n) SW_INL {
     const uint16_t* pp = vr + (n / (D / 32)) * 16 * L::VS + (n % (D / 32)) * 32;
     const i16x4 r0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
         (__attribute__((address_space(3))) i16x4*)(pp));
@@ -411,118 +323,113 @@ __global__ __launch_bounds__(256, 1) void attn_prefill_bf16_kernel(
         (__attribute__((address_space(3))) i16x4*)(pp + 8 * L::VS));
     return __builtin_bit_cast(bf16x8, __builtin_shufflevector(r0, r1, 0, 1, 2, 3, 4, 5, 6, 7));
   };
+  // O^T += V^T P^T for the 16-key chunks c0, c0+1 of a tile (not pipelined)
+  auto pv_sub = [&](const uint16_t* vs, const uint32_t (&w0)[4], const uint32_t (&w1)[4], int c0) SW_INL {
+    const uint16_t* vr = vs + vlane + c0 * 16 * L::VS;
+    const bf16x8 pb[2] = {__builtin_bit_cast(bf16x8, w0), __builtin_bit_cast(bf16x8, w1)};
+#pragma unroll
+    for (int n = 0; n < NPV; ++n)
+      oacc[n % (D / 32)] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vread(vr, n), pb[n / (D / 32)],
+                                                                   oacc[n % (D / 32)], 0, 0, 0);
+  };
   // rare path: exact row max of S, new reference, rescale, recompute P(u)
-  auto refix = [&](f32x16 (&S)[2], uint32_t (&w0)[2][4], uint32_t (&w1)[2][4], float (&ts)[2])
-      __attribute__((always_inline)) {
-    float mx[2];
-    row_max(S, mx);
+  auto refix = [&](const f32x16& S, uint32_t (&w0)[4], uint32_t (&w1)[4], float& ts) SW_INL {
+    rescale_to(fmaxf(mref, row_max(S)));
+    ts = 0.0f;
 #pragma unroll
-    for (int qh = 0; qh < 2; ++qh) {
-      const float nref = fmaxf(mref[qh], mx[qh]);
-      const float alpha = __builtin_amdgcn_exp2f(mref[qh] - nref);
-      mref[qh] = nref;
-      lsum[qh] *= alpha;
+    for (int e = 0; e < 4; ++e) pair(S, e, w0[e], ts);
 #pragma unroll
-      for (int td = 0; td < D / 32; ++td)
-#pragma unroll
-        for (int j = 0; j < 16; ++j) oacc[qh][td][j] *= alpha;
-      ts[qh] = 0.0f;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) pair(S, qh, e, w0[qh][e], ts[qh]);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) pair(S, qh, 4 + e, w1[qh][e], ts[qh]);
-    }
+    for (int e = 0; e < 4; ++e) pair(S, 4 + e, w1[e], ts);
   };
-  // check of P(u) between the phases; adds its sums
-  auto check = [&](f32x16 (&cur)[2], uint32_t (&w0)[2][4], uint32_t (&w1)[2][4], float (&ts)[2])
-      __attribute__((always_inline)) {
-    if (__any(ts[0] > kSumLimit || ts[1] > kSumLimit)) refix(cur, w0, w1, ts);
-    lsum[0] += ts[0];
-    lsum[1] += ts[1];
+  auto check = [&](const f32x16& cur, uint32_t (&w0)[4], uint32_t (&w1)[4], float& ts) SW_INL {
+    if (__any(ts > kSumLimit)) refix(cur, w0, w1, ts);
+    lsum += ts;
   };
-  // phase B: P.V of sub-step u (words w0: chunk 0, w1: chunk 1), with the
-  // chunk-0 exponentials of the next sub-step's scores when HAS_NEXT
-  auto phase_b = [&](const uint16_t* vr, uint32_t (&w0)[2][4], uint32_t (&w1)[2][4],
-                     bf16x8 (&vf)[NPV], f32x16 (&nxt)[2], uint32_t (&wn)[2][4], float (&tn)[2],
-                     auto has_next) __attribute__((always_inline)) {
+  // phase B: P.V of sub-tile u, with the chunk-0 exponentials of the next
+  // sub-tile's scores when HAS_NEXT
+  auto phase_b = [&](const uint16_t* vr, const uint32_t (&w0)[4], const uint32_t (&w1)[4],
+                     bf16x8 (&vf)[NPV], const f32x16& nxt, uint32_t (&wn)[4], float& tn,
+                     auto has_next) SW_INL {
     constexpr bool HAS_NEXT = decltype(has_next)::value;
-    bf16x8 pb[2][2];
-#pragma unroll
-    for (int qh = 0; qh < 2; ++qh) {
-      pb[qh][0] = __builtin_bit_cast(bf16x8, w0[qh]);
-      pb[qh][1] = __builtin_bit_cast(bf16x8, w1[qh]);
-    }
-    tn[0] = 0.0f;
-    tn[1] = 0.0f;
+    const bf16x8 pb[2] = {__builtin_bit_cast(bf16x8, w0), __builtin_bit_cast(bf16x8, w1)};
+    tn = 0.0f;
 #pragma unroll
     for (int n = 0; n < NPV; ++n) {
       if (n + 2 < NPV) vf[n + 2] = vread(vr, n + 2);
-      const int cc = n / (D / 32), td = n % (D / 32);
-#pragma unroll
-      for (int qh = 0; qh < 2; ++qh) {
-        oacc[qh][td] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[n], pb[qh][cc], oacc[qh][td], 0, 0, 0);
-        const int m = n * 2 + qh;
-        if (HAS_NEXT && (m % PV_PER_PAIR) == PV_PER_PAIR - 1) {
-          const int pr = m / PV_PER_PAIR;              // 0..7
-          pair(nxt, pr / 4, pr % 4, wn[pr / 4][pr % 4], tn[pr / 4]);
-        }
-        __builtin_amdgcn_sched_barrier(0);
+      oacc[n % (D / 32)] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[n], pb[n / (D / 32)],
+                                                                   oacc[n % (D / 32)], 0, 0, 0);
+      if (HAS_NEXT && (n % PV_PER_PAIR) == PV_PER_PAIR - 1) {
+        const int e = n / PV_PER_PAIR;               // 0..3
+        pair(nxt, e, wn[e], tn);
       }
+      __builtin_amdgcn_sched_barrier(0);
     }
   };
-  auto sub = [&](f32x16 (&cur)[2], uint32_t (&wc)[2][4], float (&tc)[2], f32x16 (&nxt)[2],
-                 uint32_t (&wn)[2][4], float (&tn)[2], const uint16_t* ksn, int h2n,
-                 const uint16_t* vs, int c0) __attribute__((always_inline)) {
+  // One pipeline sub-step (see the header): cur = S(u) with chunk-0 words wc
+  // and their partial sum tc; produces nxt = S(u+1), its chunk-0 words wn and
+  // partial sum tn.
+  auto sub = [&](f32x16& cur, uint32_t (&wc)[4], float& tc, f32x16& nxt, uint32_t (&wn)[4],
+                 float& tn, const uint16_t* ksn, int h2n, const uint16_t* vs, int c0) SW_INL {
     const uint16_t* kr = ksn + (h2n * 32 + ln) * L::KS + hl * 8;
     const uint16_t* vr = vs + vlane + c0 * 16 * L::VS;
-    uint32_t w1[2][4];
+    uint32_t w1[4];
     bf16x8 kf[NKK];
     bf16x8 vf[NPV];
     kf[0] = *reinterpret_cast<const bf16x8*>(kr);
     kf[1] = *reinterpret_cast<const bf16x8*>(kr + 16);
 #pragma unroll
-    for (int qh = 0; qh < 2; ++qh)
-#pragma unroll
-      for (int j = 0; j < 16; ++j) nxt[qh][j] = 0.0f;
+    for (int j = 0; j < 16; ++j) nxt[j] = 0.0f;
 #pragma unroll
     for (int kk = 0; kk < NKK; ++kk) {
       if (kk + 2 < NKK) kf[kk + 2] = *reinterpret_cast<const bf16x8*>(kr + (kk + 2) * 16);
       if (kk == NKK - 2) vf[0] = vread(vr, 0);
       if (kk == NKK - 1) vf[1] = vread(vr, 1);
-#pragma unroll
-      for (int qh = 0; qh < 2; ++qh) {
-        nxt[qh] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[kk], qf[qh][kk], nxt[qh], 0, 0, 0);
-        const int m = kk * 2 + qh;
-        if ((m % QK_PER_PAIR) == QK_PER_PAIR - 1) {
-          const int pr = m / QK_PER_PAIR;              // 0..7
-          pair(cur, pr / 4, 4 + pr % 4, w1[pr / 4][pr % 4], tc[pr / 4]);
-        }
-        __builtin_amdgcn_sched_barrier(0);
+      nxt = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[kk], qf[kk], nxt, 0, 0, 0);
+      if ((kk % QK_PER_PAIR) == QK_PER_PAIR - 1) {
+        const int e = kk / QK_PER_PAIR;              // 0..3
+        pair(cur, 4 + e, w1[e], tc);
       }
+      __builtin_amdgcn_sched_barrier(0);
     }
     check(cur, wc, w1, tc);
     phase_b(vr, wc, w1, vf, nxt, wn, tn, std::true_type{});
   };
   // final sub-step of the off-diagonal run: no scores ahead
-  auto sub_last = [&](f32x16 (&cur)[2], uint32_t (&wc)[2][4], float (&tc)[2],
-                      const uint16_t* vs, int c0) __attribute__((always_inline)) {
+  auto sub_last = [&](f32x16& cur, uint32_t (&wc)[4], float& tc, const uint16_t* vs, int c0) SW_INL {
     const uint16_t* vr = vs + vlane + c0 * 16 * L::VS;
-    uint32_t w1[2][4];
+    uint32_t w1[4];
     bf16x8 vf[NPV];
     vf[0] = vread(vr, 0);
     vf[1] = vread(vr, 1);
 #pragma unroll
-    for (int pr = 0; pr < 8; ++pr) pair(cur, pr / 4, 4 + pr % 4, w1[pr / 4][pr % 4], tc[pr / 4]);
+    for (int e = 0; e < 4; ++e) pair(cur, 4 + e, w1[e], tc);
     check(cur, wc, w1, tc);
-    float tdummy[2];
-    phase_b(vr, wc, w1, vf, cur, wc, tdummy, std::false_type{});
+    uint32_t wdummy[4];
+    float tdummy;
+    phase_b(vr, wc, w1, vf, cur, wdummy, tdummy, std::false_type{});
   };
-  f32x16 sX[2], sY[2];
-  uint32_t wX[2][4], wY[2][4];
-  float tX[2], tY[2];
+
+  // Stages: during tile step t, K/V(t) are in stv, K(t+1) in stk, and tile
+  // t+2 is written to stw from the registers loaded during step t-1; tile
+  // t+3 is loaded into those registers.
+  int stv = 0, stk = 1, stw = 2;
+  auto stage_io = [&](int t) SW_INL {
+    if (t + 2 < ntiles) store_tile(stw);
+    if (t + 3 < ntiles) load_tile(t + 3);
+  };
+  auto next_stage = [&]() SW_INL {
+    const int t0 = stv;
+    stv = stk;
+    stk = stw;
+    stw = t0;
+    __syncthreads();
+  };
+  f32x16 sX, sY;
+  uint32_t wX[4], wY[4];
+  float tX = 0.0f, tY = 0.0f;
   // off-diagonal tile t < nofft-1: both halves, the second computing the
   // first half of tile t+1
-  auto tile_step = [&](int t) __attribute__((always_inline)) {
+  auto tile_step = [&](int t) SW_INL {
     stage_io(t);
     const uint16_t* kt = lds + stv * L::STAGE;
     const uint16_t* vs = kt + L::K_ELEMS;
@@ -530,7 +437,7 @@ __global__ __launch_bounds__(256, 1) void attn_prefill_bf16_kernel(
     sub(sY, wY, tY, sX, wX, tX, lds + stk * L::STAGE, 0, vs, 2);
     next_stage();
   };
-  auto tile_last = [&](int t) __attribute__((always_inline)) {
+  auto tile_last = [&](int t) SW_INL {
     stage_io(t);
     const uint16_t* kt = lds + stv * L::STAGE;
     const uint16_t* vs = kt + L::K_ELEMS;
@@ -539,7 +446,7 @@ __global__ __launch_bounds__(256, 1) void attn_prefill_bf16_kernel(
     next_stage();
   };
   // diagonal-block tile, not pipelined: scores, mask, max, P, P.V per half
-  auto tile_diag = [&](int t) __attribute__((always_inline)) {
+  auto tile_diag = [&](int t) SW_INL {
     stage_io(t);
     const uint16_t* kt = lds + stv * L::STAGE;
     const uint16_t* vs = kt + L::K_ELEMS;
@@ -547,10 +454,16 @@ __global__ __launch_bounds__(256, 1) void attn_prefill_bf16_kernel(
     for (int h2 = 0; h2 < 2; ++h2) {
       qk_sub(kt, h2, sX);
       mask_sub(t, h2, sX);
-      update_ref(sX);
-      bf16x8 pb[2][2];
-      softmax_sub(sX, pb);
-      pv_sub(vs, pb, 2 * h2);
+      const float mx = row_max(sX);
+      if (__any(mx > mref + kRescaleSlack)) rescale_to(mx > mref + kRescaleSlack ? mx : mref);
+      uint32_t w0[4], w1[4];
+      float ts = 0.0f;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) pair(sX, e, w0[e], ts);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) pair(sX, 4 + e, w1[e], ts);
+      lsum += ts;
+      pv_sub(vs, w0, w1, 2 * h2);
     }
     next_stage();
   };
@@ -566,15 +479,12 @@ __global__ __launch_bounds__(256, 1) void attn_prefill_bf16_kernel(
     __syncthreads();
     int t = 0;
     if (nofft > 0) {
-      // scores of the first half tile; its chunk-0 words are left to the
+      // scores of the first sub-tile; its chunk-0 words are left to the
       // first check (an infinite partial sum forces the exact reference)
       qk_sub(lds, 0, sX);
+      tX = INFINITY;
 #pragma unroll
-      for (int qh = 0; qh < 2; ++qh) {
-        tX[qh] = INFINITY;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) wX[qh][e] = 0u;
-      }
+      for (int e = 0; e < 4; ++e) wX[e] = 0u;
       for (; t + 1 < nofft; ++t) tile_step(t);
       tile_last(t);
       ++t;
@@ -583,32 +493,26 @@ __global__ __launch_bounds__(256, 1) void attn_prefill_bf16_kernel(
   }
 
   // ---- epilogue ----
-  float ltot[2];
+  const float ltot = sum_other_half(lsum);
+  if (!active || qpos >= seq1) return;
+  const float inv = ltot > 0.0f ? 1.0f / ltot : 0.0f;
+  uint16_t* orow = O + ((long long)u * N + qpos) * D;
 #pragma unroll
-  for (int qh = 0; qh < 2; ++qh) ltot[qh] = sum_other_half(lsum[qh]);
-  if (!active) return;
+  for (int td = 0; td < D / 32; ++td) {
 #pragma unroll
-  for (int qh = 0; qh < 2; ++qh) {
-    const int qpos = q0 + qh * 32 + ln;
-    if (qpos >= seq1) continue;
-    const float inv = ltot[qh] > 0.0f ? 1.0f / ltot[qh] : 0.0f;
-    uint16_t* orow = O + ((long long)u * N + qpos) * D;
-#pragma unroll
-    for (int td = 0; td < D / 32; ++td) {
-#pragma unroll
-      for (int jb = 0; jb < 4; ++jb) {
-        const int dv = td * 32 + jb * 8 + hl * 4;
-        uint2 st;
-        st.x = pack_bf16x2(oacc[qh][td][jb * 4 + 0] * inv, oacc[qh][td][jb * 4 + 1] * inv);
-        st.y = pack_bf16x2(oacc[qh][td][jb * 4 + 2] * inv, oacc[qh][td][jb * 4 + 3] * inv);
-        *reinterpret_cast<uint2*>(orow + dv) = st;
-      }
+    for (int jb = 0; jb < 4; ++jb) {
+      const int dv = td * 32 + jb * 8 + hl * 4;
+      uint2 st;
+      st.x = pack_bf16x2(oacc[td][jb * 4 + 0] * inv, oacc[td][jb * 4 + 1] * inv);
+      st.y = pack_bf16x2(oacc[td][jb * 4 + 2] * inv, oacc[td][jb * 4 + 3] * inv);
+      *reinterpret_cast<uint2*>(orow + dv) = st;
     }
-    if (lse && hl == 0)
-      lse[(long long)u * N + qpos] =
-          (ltot[qh] > 0.0f) ? (mref[qh] + log2f(ltot[qh])) / kLog2e : -INFINITY;
   }
+  if (lse && hl == 0)
+    lse[(long long)u * N + qpos] = (ltot > 0.0f) ? (mref + log2f(ltot)) / kLog2e : -INFINITY;
 }
+
+#undef SW_INL
 
 // ---------------------------------------------------------------------------
 // fp32 kernel
@@ -771,15 +675,15 @@ hipError_t launch_attn_prefill(int dtype, const void* Q, const void* K, const vo
   const int groups = (int)(nb * h_kv);
   const float sl2 = scale * kLog2e;
   if (dtype == SW_BF16) {
-    // 64 query rows per wavefront, 4 wavefronts per workgroup
-    const int sg = (G * (meta.B / 64) + 3) / 4;
+    // 32 query rows per wavefront, kPfWaves wavefronts per workgroup
+    const int sg = (G * (meta.B / 32) + kPfWaves - 1) / kPfWaves;
     const unsigned grid = (unsigned)(((groups + 7) / 8) * 8 * sg);
     auto q = reinterpret_cast<const uint16_t*>(Q);
     auto k = reinterpret_cast<const uint16_t*>(K);
     auto v = reinterpret_cast<const uint16_t*>(V);
     auto o = reinterpret_cast<uint16_t*>(O);
 #define SW_LAUNCH_BF16(DD, BB)                                                                  \
-  hipLaunchKernelGGL((attn_prefill_bf16_kernel<DD, BB>), dim3(grid), dim3(256), 0, st, q, k, v, h_q, \
+  hipLaunchKernelGGL((attn_prefill_bf16_kernel<DD, BB>), dim3(grid), dim3(kPfWaves * 64), 0, st, q, k, v, h_q, \
                      h_kv, N, meta, idx, cnt, kmax, sl2, o, lse, groups, sg)
     if (d == 128 && meta.B == 128) SW_LAUNCH_BF16(128, 128);
     else if (d == 128) SW_LAUNCH_BF16(128, 64);
