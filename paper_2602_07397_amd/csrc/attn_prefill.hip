@@ -218,16 +218,16 @@ __global__ __launch_bounds__(kPfWaves * 64, 1) void attn_prefill_bf16_kernel(
   }
   const uint16_t* Kg = K + (long long)g * N * D;
   const uint16_t* Vg = V + (long long)g * N * D;
+  // first key of tile t (wave-uniform)
   auto tile_k0 = [&](int t) SW_INL {
     const int jj = t / TPB;
-    const int j = (jj < n_off) ? blist[jj] : i;
+    const int j = (jj < n_off) ? __builtin_amdgcn_readfirstlane(blist[jj]) : i;
     return seq0 + j * BLK + (t % TPB) * KT;
   };
-  // Raw buffer loads through a descriptor based at the tile's first key and
-  // sized to the end of the sequence: keys past the end read as zero without
-  // per-lane tests (the diagonal-tile mask removes them).
-  auto load_tile = [&](int t) SW_INL {
-    const int k0 = tile_k0(t);
+  // Raw buffer loads through a descriptor based at the tile's first key k0
+  // and sized to the end of the sequence: keys past the end read as zero
+  // without per-lane tests (the diagonal-tile mask removes them).
+  auto load_tile_at = [&](int k0) SW_INL {
     const int bytes = max(0, (seq1 - k0) * D * 2);
     const __amdgpu_buffer_rsrc_t rk =
         __builtin_amdgcn_make_buffer_rsrc((void*)(Kg + (long long)k0 * D), (short)0, bytes, kBufWord3);
@@ -241,6 +241,7 @@ __global__ __launch_bounds__(kPfWaves * 64, 1) void attn_prefill_bf16_kernel(
       vreg[p] = __builtin_bit_cast(uint4, b);
     }
   };
+  auto load_tile = [&](int t) SW_INL { load_tile_at(tile_k0(t)); };
   auto store_tile = [&](int st) SW_INL {
     uint16_t* ks = lds + st * L::STAGE;
     uint16_t* vs = ks + L::K_ELEMS;
@@ -412,10 +413,14 @@ __global__ __launch_bounds__(kPfWaves * 64, 1) void attn_prefill_bf16_kernel(
   // Stages: during tile step t, K/V(t) are in stv, K(t+1) in stk, and tile
   // t+2 is written to stw from the registers loaded during step t-1; tile
   // t+3 is loaded into those registers.
+  // The first key of tile t+3 is looked up one step ahead (k0_ahead), so the
+  // LDS read of the block list never stalls the loads.
   int stv = 0, stk = 1, stw = 2;
+  int k0_ahead = 0;
   auto stage_io = [&](int t) SW_INL {
     if (t + 2 < ntiles) store_tile(stw);
-    if (t + 3 < ntiles) load_tile(t + 3);
+    if (t + 3 < ntiles) load_tile_at(k0_ahead);
+    if (t + 4 < ntiles) k0_ahead = tile_k0(t + 4);
   };
   auto next_stage = [&]() SW_INL {
     const int t0 = stv;
@@ -476,6 +481,7 @@ __global__ __launch_bounds__(kPfWaves * 64, 1) void attn_prefill_bf16_kernel(
       store_tile(1);
     }
     if (ntiles > 2) load_tile(2);
+    if (ntiles > 3) k0_ahead = tile_k0(3);
     __syncthreads();
     int t = 0;
     if (nofft > 0) {
