@@ -552,7 +552,9 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(const T* __restrict__ 
 
 // bf16 split-K decode attention on MFMA. Workgroup = (sequence, KV head,
 // split), 4 wavefronts; a wavefront takes groups of 16 consecutive selected
-// tokens (2 groups per step, all loads issued first).
+// tokens, GPS groups per step, loading the groups of step it+1 while it
+// computes step it (two register sets, the step loop unrolled by two so
+// neither set is copied).
 //   S = K q^T   v_mfma_f32_16x16x32_bf16: A = 16 key rows x 32 dims read
 //               straight from the cache (16 bytes per lane), B = the G query
 //               heads (zero-padded to 16 columns). Lane n + 16 (m / 4) holds
@@ -561,9 +563,15 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(const T* __restrict__ 
 //   O^T += V^T P^T  v_mfma_f32_16x16x16bf16_1k: A = V^T from a per-wave LDS
 //               slice written transposed (4 keys x 8 dims per lane), B = P in
 //               the accumulator layout of S.
+// The split's block indices are staged in LDS once, and the K/V loads go
+// through buffer descriptors that end at the last valid token (lanes past it
+// read zero), so the loop has no global index loads and no per-lane branches
+// around loads: the loads of the next step stay in flight during the math.
 typedef __bf16 bf16x8d __attribute__((ext_vector_type(8)));
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4d __attribute__((ext_vector_type(4)));
+
+constexpr int kDecBufWord3 = 0x00020000;   // raw buffer descriptor word 3 (gfx9 family)
 
 template <int D>
 __global__ __launch_bounds__(256) void attn_decode_mfma_kernel(
@@ -577,6 +585,7 @@ __global__ __launch_bounds__(256) void attn_decode_mfma_kernel(
   constexpr int VT_BYTES = 4 * GPS * D * VTS * 2;
   constexpr int EP_BYTES = (4 * 16 * D + 2 * 4 * 16) * 4;
   __shared__ __attribute__((aligned(16))) char smem[VT_BYTES > EP_BYTES ? VT_BYTES : EP_BYTES];
+  __shared__ int16_t ssel[SW_MAX_BLOCKS + 2];      // this split's block indices
   auto vt_slice = [&](int wv, int x) {
     return reinterpret_cast<uint16_t*>(smem) + (wv * GPS + x) * D * VTS;
   };
@@ -589,15 +598,22 @@ __global__ __launch_bounds__(256) void attn_decode_mfma_kernel(
   const int g = bg % h_kv;
   const int h_q = h_kv * G;
   const int tid = threadIdx.x;
-  const int w = tid >> 6, l = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6), l = tid & 63;
   const int ln = l & 15, lg = l >> 4;
   const int p = pos[bi];
   const bool ok = p >= 0 && p < T_max;
   const int bc = ok ? p / B : 0;
-  const int tau = ok ? max(0, min(cnt[bi], kmax)) : 0;
-  const int ngroups = tau * (B / 16);
+  // a valid selection has at most SW_MAX_BLOCKS distinct blocks
+  const int tau = ok ? max(0, min(min(cnt[bi], kmax), SW_MAX_BLOCKS)) : 0;
+  const int gpb = B / 16;                          // 16-token groups per block
+  const int ngroups = tau * gpb;
   const int g0 = (int)((long long)ngroups * sp / S), g1 = (int)((long long)ngroups * (sp + 1) / S);
-  const int32_t* sel = idx + (long long)bi * kmax;
+  const int jlo = g0 / gpb;
+  const int nj = (g1 > g0) ? (g1 - 1) / gpb - jlo + 1 : 0;
+  {
+    const int32_t* sel = idx + (long long)bi * kmax + jlo;
+    for (int e = tid; e < nj; e += 256) ssel[e] = (int16_t)max(-1, min(sel[e], 32767));
+  }
 
   // query fragments (B operand of S = K q^T): head ln, dims 32c + 8 lg .. +7
   bf16x8d qf[D / 32];
@@ -619,52 +635,53 @@ __global__ __launch_bounds__(256) void attn_decode_mfma_kernel(
   // V staging: lane takes keys 4 kq .. 4 kq + 3 and dims 8 dq .. 8 dq + 7
   const int kq = l & 3, dq = l >> 2;
   const bool vthr = dq < D / 8;
+  // per-lane byte offsets inside a 16-token group (tile invariant)
+  const int koff = ln * D * 2 + lg * 16;
+  const int voff = vthr ? (kq * 4 * D * 2 + dq * 16) : 0x40000000;   // idle lanes read past the end
+  __syncthreads();                                 // ssel visible
 
   const int nsteps = (g1 - g0 + 4 * GPS - 1) / (4 * GPS);
-  // Register double buffering: the loads of step it+1 are issued before the
-  // math of step it.
-  uint4 kraw[GPS][D / 32], vraw[GPS][4];
-  uint4 nk[GPS][D / 32], nvv[GPS][4];
-  int tok0[GPS], ntok[GPS];
-  bool gvalid[GPS], nvalid[GPS];
-  auto issue = [&](int step, uint4 (&kr)[GPS][D / 32], uint4 (&vr)[GPS][4], int (&t0s)[GPS],
-                   bool (&vals)[GPS]) {
+  // token of the first key of group gi, or -1 when the group holds no valid key
+  auto group_t0 = [&](int gi) {
+    const int f = gi * 16;
+    const int jj = f / B;
+    const int j = __builtin_amdgcn_readfirstlane((int)ssel[jj - jlo]);
+    const int t0 = j * B + (f - jj * B);
+    return __builtin_amdgcn_readfirstlane((j >= 0 && j <= bc && t0 <= p) ? t0 : -1);
+  };
+  auto issue = [&](int step, uint4 (&kr)[GPS][D / 32], uint4 (&vr)[GPS][4], int (&t0s)[GPS]) {
 #pragma unroll
     for (int x = 0; x < GPS; ++x) {
       const int gi = g0 + (step * 4 + w) * GPS + x;
-      bool v = step < nsteps && gi < g1;
-      int t0 = 0;
-      if (v) {
-        const int f = gi * 16;
-        const int jj = f / B;
-        const int j = sel[jj];
-        t0 = j * B + (f - jj * B);
-        v = (j >= 0 && j <= bc && t0 <= p);
-      }
-      vals[x] = v;
+      const int t0 = (step < nsteps && gi < g1) ? group_t0(gi) : -1;
       t0s[x] = t0;
-      const int key = t0 + ln;
-      const bool kv = v && key <= p;
+      // No branch around the loads (the wait counts stay exact): a group
+      // without valid keys gets an empty descriptor and reads zeros.
+      const int tb = max(t0, 0);
+      const int bytes = (t0 >= 0) ? (p + 1 - t0) * D * 2 : 0;   // keys past p read as zero
+      const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc(
+          (void*)(Kb + (long long)tb * D), (short)0, bytes, kDecBufWord3);
+      const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc(
+          (void*)(Vb + (long long)tb * D), (short)0, bytes, kDecBufWord3);
 #pragma unroll
-      for (int c = 0; c < D / 32; ++c)
-        kr[x][c] = kv ? *reinterpret_cast<const uint4*>(Kb + (long long)key * D + 32 * c + lg * 8)
-                      : make_uint4(0, 0, 0, 0);
+      for (int c = 0; c < D / 32; ++c) {
+        auto a = __builtin_amdgcn_raw_buffer_load_b128(rk, koff + c * 64, 0, 0);
+        kr[x][c] = __builtin_bit_cast(uint4, a);
+      }
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int vk = t0 + kq * 4 + r;
-        vr[x][r] = (v && vthr && vk <= p)
-                       ? *reinterpret_cast<const uint4*>(Vb + (long long)vk * D + dq * 8)
-                       : make_uint4(0, 0, 0, 0);
+        auto b = __builtin_amdgcn_raw_buffer_load_b128(rv, voff + r * D * 2, 0, 0);
+        vr[x][r] = __builtin_bit_cast(uint4, b);
       }
     }
   };
-  issue(0, kraw, vraw, tok0, gvalid);
-  for (int it = 0; it < nsteps; ++it) {
-    issue(it + 1, nk, nvv, ntok, nvalid);
+  // one step on the register set (kraw, vraw, tok0)
+  auto compute = [&](const uint4 (&kraw)[GPS][D / 32], const uint4 (&vraw)[GPS][4],
+                     const int (&tok0)[GPS]) {
     // V^T into this wave's LDS slice
 #pragma unroll
     for (int x = 0; x < GPS; ++x) {
-      if (vthr) {
+      if (vthr && tok0[x] >= 0) {
         uint16_t* vt = vt_slice(w, x);
         const uint32_t a[4] = {vraw[x][0].x, vraw[x][0].y, vraw[x][0].z, vraw[x][0].w};
         const uint32_t b[4] = {vraw[x][1].x, vraw[x][1].y, vraw[x][1].z, vraw[x][1].w};
@@ -687,11 +704,11 @@ __global__ __launch_bounds__(256) void attn_decode_mfma_kernel(
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 #pragma unroll
     for (int x = 0; x < GPS; ++x) {
-      if (!gvalid[x]) continue;                    // uniform across the wavefront
+      if (tok0[x] < 0) continue;                   // uniform across the wavefront
       f32x4d sacc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int c = 0; c < D / 32; ++c)
-        sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(*reinterpret_cast<bf16x8d*>(&kraw[x][c]),
+        sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8d, kraw[x][c]),
                                                        qf[c], sacc, 0, 0, 0);
       float sv[4];
       float mx = -INFINITY;
@@ -731,15 +748,16 @@ __global__ __launch_bounds__(256) void attn_decode_mfma_kernel(
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-#pragma unroll
-    for (int x = 0; x < GPS; ++x) {
-#pragma unroll
-      for (int c = 0; c < D / 32; ++c) kraw[x][c] = nk[x][c];
-#pragma unroll
-      for (int r = 0; r < 4; ++r) vraw[x][r] = nvv[x][r];
-      tok0[x] = ntok[x];
-      gvalid[x] = nvalid[x];
-    }
+  };
+  uint4 kA[GPS][D / 32], vA[GPS][4], kB[GPS][D / 32], vB[GPS][4];
+  int tA[GPS], tB[GPS];
+  issue(0, kA, vA, tA);
+  for (int it = 0; it < nsteps; it += 2) {
+    issue(it + 1, kB, vB, tB);
+    compute(kA, vA, tA);
+    if (it + 1 >= nsteps) break;
+    issue(it + 2, kA, vA, tA);
+    compute(kB, vB, tB);
   }
   __syncthreads();                                 // V^T slices are dead from here
   // per-wave partials: head ln; lane groups hold disjoint keys (sum l) and
