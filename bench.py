@@ -38,10 +38,10 @@ PEAK_HBM_GBS = 8000.0
 # measured on: a changed source reports null.
 FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
 MEASURED_TRAFFIC = {
-    "attn_prefill.hip": ("760d6a0d7885933cb9d0c8374a7f3a3eb5708ef8ad78259050b90255cd30fecd",
-                         332728.4 * 1024, 262164.2 * 1024),
-    "decode.hip": ("465e1f887da5ea36d53e3959803a7b21e1431d02dc50d621b5acbf180ffe767b",
-                   418341.1 * 1024, 1088.0 * 1024),
+    "attn_prefill.hip": ("5b49ac6e694ecec9bedc4ed002e1eb398cd5ae98dcef25c275efcc8f653ea851",
+                         334395.8 * 1024, 262144.0 * 1024),
+    "decode.hip": ("2d82dfaa0e5b8ba66507ccf21dc81a4486d589f6a3bb8efbed0912d3030a4ee5",
+                   418574.4 * 1024, 1088.0 * 1024),
 }
 
 
