@@ -224,6 +224,7 @@ int sw_kv_append(int dtype, const void* k_new, const void* v_new, void* Kc, void
  *     (ii) last column A[m][b_cur] = Qs[m] . Ks[b_cur] / sqrt(r), m <= b_cur
  *     (the diagonal entry comes from (ii)).
  * signs/cols/r as in sw_sketch_scores (same transform as the prompt).
+ * q_new and k_new must be 16-byte aligned (SW_ERR_INVALID_ARG otherwise).
  */
 int sw_sketch_scores_decode(int dtype, const void* q_new, const void* k_new, int batch, int h_q,
                             int h_kv, int d, int B, const int32_t* pos, const int8_t* signs,

@@ -339,8 +339,8 @@ int sw_sketch_scores_decode(int dtype, const void* q_new, const void* k_new, int
   if (dtype != SW_F32 && dtype != SW_BF16) return fail(SW_ERR_INVALID_ARG, "dtype=%d", dtype);
   CHECK(check_heads(h_q, h_kv));
   CHECK(check_decode_shape(batch, d, r, b_max, B));
-  CHECK(check_ptr(q_new, 4, "q_new"));
-  CHECK(check_ptr(k_new, 4, "k_new"));
+  CHECK(check_ptr(q_new, 16, "q_new"));
+  CHECK(check_ptr(k_new, 16, "k_new"));
   CHECK(check_ptr(pos, 4, "pos"));
   CHECK(check_ptr(signs, 1, "signs"));
   CHECK(check_ptr(cols, 4, "cols"));

@@ -138,8 +138,9 @@ __global__ __launch_bounds__(256) void decode_reps_kernel(const T* __restrict__ 
                                                           const int32_t* __restrict__ cols, int r,
                                                           int batch, int b_max,
                                                           char* __restrict__ state) {
+  constexpr int V = 16 / (int)sizeof(T);             // elements per 16-byte load
   __shared__ double xq[256], xk[256], xb[256];
-  __shared__ double pq[256], pk[256];
+  __shared__ double pq[256 * V], pk[256 * V];
   const DecodeLayout L = decode_layout(batch, d, r, b_max);
   const int bi = blockIdx.x;
   const int t = threadIdx.x;
@@ -151,14 +152,29 @@ __global__ __launch_bounds__(256) void decode_reps_kernel(const T* __restrict__ 
   double* Qs = reinterpret_cast<double*>(state + L.qs) + (long long)bi * b_max * r;
   double* Ks = reinterpret_cast<double*>(state + L.ks) + (long long)bi * b_max * r;
   double* qt = reinterpret_cast<double*>(state + L.qt) + (long long)bi * r;
-  // head sums: thread (part, dim) adds the heads u = part, part + P, ...
-  const int P = 256 / d;
-  const int dim = t % d, part = t / d;
-  double sq = 0.0, sk = 0.0;
-  for (int u = part; u < h_q; u += P) sq += (double)load_f32(q_new, ((long long)bi * h_q + u) * d + dim);
-  for (int g = part; g < h_kv; g += P) sk += (double)load_f32(k_new, ((long long)bi * h_kv + g) * d + dim);
-  pq[t] = sq;
-  pk[t] = sk;
+  // head sums: thread (group, chunk) adds the 16-byte chunk `chunk` (V dims)
+  // of the heads u = group, group + P, ...; then the P groups are added per dim
+  const int dpc = d / V;                           // chunks per head row
+  const int P = 256 / dpc;                         // head groups
+  const int ch = t % dpc, grp = t / dpc;
+  double sq[V], sk[V];
+#pragma unroll
+  for (int e = 0; e < V; ++e) sq[e] = sk[e] = 0.0;
+  auto add_chunk = [&](const T* src, double (&acc)[V]) {
+    const uint4 raw = *reinterpret_cast<const uint4*>(src);
+    const T* v = reinterpret_cast<const T*>(&raw);
+#pragma unroll
+    for (int e = 0; e < V; ++e) acc[e] += (double)load_f32(v, e);
+  };
+#pragma unroll 4
+  for (int u = grp; u < h_q; u += P) add_chunk(q_new + ((long long)bi * h_q + u) * d + ch * V, sq);
+#pragma unroll 4
+  for (int g = grp; g < h_kv; g += P) add_chunk(k_new + ((long long)bi * h_kv + g) * d + ch * V, sk);
+#pragma unroll
+  for (int e = 0; e < V; ++e) {
+    pq[grp * d + ch * V + e] = sq[e];
+    pk[grp * d + ch * V + e] = sk[e];
+  }
   const bool fresh = (p % B) == 0;
   const int qc = cnt[0], kc = cnt[1];
   __syncthreads();
