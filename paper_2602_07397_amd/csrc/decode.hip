@@ -243,27 +243,29 @@ __global__ __launch_bounds__(256) void decode_scores_kernel(const int32_t* __res
   const double* qt = reinterpret_cast<const double*>(state + L.qt) + (long long)bi * r;
   float* A = reinterpret_cast<float*>(state + L.a) + (long long)bi * b_max * L.lda;
   const double rs = 1.0 / sqrt((double)r);
+  // four threads per row j (kScoreChunk rows per workgroup); thread q4 takes
+  // the sketch coordinates k = 4 i + q4, all loads independent
   const int t = threadIdx.x;
-  const int sub = t & 15, rr = t >> 4;
-  for (int pass = 0; pass < kScoreChunk / 16; ++pass) {
-    const int j = r0 + pass * 16 + rr;
-    double accr = 0.0, accc = 0.0;
-    if (j <= bc) {
-      for (int k = sub; k < r; k += 16) {
-        const double kb = Ks[(long long)bc * r + k];
-        accc += Qs[(long long)j * r + k] * kb;
-        if (j < bc) accr += qt[k] * Ks[(long long)j * r + k];
-      }
+  const int q4 = t & 3;
+  const int j = r0 + (t >> 2);
+  double accr = 0.0, accc = 0.0;
+  if (j <= bc) {
+    const double* qsj = Qs + (long long)j * r;
+    const double* ksj = Ks + (long long)j * r;
+    const double* ksb = Ks + (long long)bc * r;
+#pragma unroll 16
+    for (int k = q4; k < r; k += 4) {
+      accc += qsj[k] * ksb[k];
+      accr += qt[k] * ksj[k];
     }
-#pragma unroll
-    for (int off = 8; off > 0; off >>= 1) {
-      accr += __shfl_xor(accr, off);
-      accc += __shfl_xor(accc, off);
-    }
-    if (sub == 0 && j <= bc) {
-      if (j < bc) A[(long long)bc * L.lda + j] = (float)(accr * rs);
-      A[(long long)j * L.lda + bc] = (float)(accc * rs);
-    }
+  }
+  accr += __shfl_xor(accr, 1);
+  accc += __shfl_xor(accc, 1);
+  accr += __shfl_xor(accr, 2);
+  accc += __shfl_xor(accc, 2);
+  if (q4 == 0 && j <= bc) {
+    if (j < bc) A[(long long)bc * L.lda + j] = (float)(accr * rs);
+    A[(long long)j * L.lda + bc] = (float)(accc * rs);
   }
 }
 
