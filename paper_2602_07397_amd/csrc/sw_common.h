@@ -64,22 +64,27 @@ __device__ __forceinline__ unsigned long long order_key(double v) {
   return (u >> 63) ? ~u : (u | 0x8000000000000000ull);
 }
 
-// Exclusive prefix sum over a 256-thread block. `tmp` holds 256 ints of LDS.
-// Returns the exclusive prefix of `v`; `*total` receives the block sum.
+// Exclusive prefix sum over a 256-thread block (4 wavefronts): an inclusive
+// scan inside each wavefront by lane shuffles, then the wavefront totals
+// through LDS. `tmp` holds at least 4 ints of LDS. Returns the exclusive
+// prefix of `v`; `*total` receives the block sum. Contains two barriers.
 __device__ __forceinline__ int block_exclusive_scan_256(int v, int* tmp, int* total) {
   const int t = threadIdx.x;
-  tmp[t] = v;
-  __syncthreads();
-  for (int off = 1; off < 256; off <<= 1) {
-    int add = (t >= off) ? tmp[t - off] : 0;
-    __syncthreads();
-    tmp[t] += add;
-    __syncthreads();
+  const int lane = t & 63, w = t >> 6;
+  int x = v;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int y = __shfl_up(x, off);
+    if (lane >= off) x += y;
   }
-  int incl = tmp[t];
-  *total = tmp[255];
+  if (lane == 63) tmp[w] = x;
   __syncthreads();
-  return incl - v;
+  int before = 0;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) before += (q < w) ? tmp[q] : 0;
+  *total = tmp[0] + tmp[1] + tmp[2] + tmp[3];
+  __syncthreads();
+  return before + x - v;
 }
 
 }  // namespace sw
