@@ -277,6 +277,7 @@ constexpr int kStrip = 32;               // columns per workgroup (8 lanes x 4)
 constexpr int kRowGroups = SW_STRIP_RG;  // row groups per workgroup
 constexpr int kStripThreads = 8 * kRowGroups;
 
+template <bool S8>   // S8: s = 8, the paper's exponent (three squarings, no loop)
 __global__ __launch_bounds__(kStripThreads) void walk_row_strip_kernel(const char* __restrict__ state,
                                                              int batch, int d, int r, int b_max,
                                                              int B, const int32_t* __restrict__ pos,
@@ -295,6 +296,14 @@ __global__ __launch_bounds__(kStripThreads) void walk_row_strip_kernel(const cha
   const double inv_c = 1.0 / (c0 > 0.0 ? c0 : 1.0);
   const int col0 = reinterpret_cast<const int32_t*>(state + L.col0)[bi];
   const float* A = reinterpret_cast<const float*>(state + L.a) + (long long)bi * b_max * L.lda;
+  auto pw = [&](double x) {
+    if constexpr (S8) {
+      const double x2 = x * x, x4 = x2 * x2;
+      return x4 * x4;
+    } else {
+      return pow_int_d(x, s_exp);
+    }
+  };
   const int t = threadIdx.x;
   const int cq = t & 7, rg = t >> 3;
   const int j = j0 + cq * 4;                       // first of this thread's 4 columns
@@ -308,7 +317,7 @@ __global__ __launch_bounds__(kStripThreads) void walk_row_strip_kernel(const cha
       const float4 a = *reinterpret_cast<const float4*>(A + (long long)bc * L.lda + j);
       const float av[4] = {a.x, a.y, a.z, a.w};
 #pragma unroll
-      for (int e = 0; e < 4; ++e) acc[e] = pow_int_d((double)av[e] * inv_c, s_exp);
+      for (int e = 0; e < 4; ++e) acc[e] = pw((double)av[e] * inv_c);
     }
   } else {
     const double* rp = r_prev + (long long)bi * b_max;
@@ -330,7 +339,7 @@ __global__ __launch_bounds__(kStripThreads) void walk_row_strip_kernel(const cha
         const float av[4] = {a[u].x, a[u].y, a[u].z, a[u].w};
 #pragma unroll
         for (int e = 0; e < 4; ++e)
-          if (j + e <= mm || j + e >= col0) acc[e] += w[u] * pow_int_d((double)av[e] * inv_c, s_exp);
+          acc[e] += (j + e <= mm || j + e >= col0) ? w[u] * pw((double)av[e] * inv_c) : 0.0;
       }
     }
     for (; m <= bc; m += kRowGroups) {
@@ -339,7 +348,7 @@ __global__ __launch_bounds__(kStripThreads) void walk_row_strip_kernel(const cha
       const float av[4] = {a.x, a.y, a.z, a.w};
 #pragma unroll
       for (int e = 0; e < 4; ++e)
-        if (j + e <= m || j + e >= col0) acc[e] += wv * pow_int_d((double)av[e] * inv_c, s_exp);
+        acc[e] += (j + e <= m || j + e >= col0) ? wv * pw((double)av[e] * inv_c) : 0.0;
     }
   }
 #pragma unroll
@@ -892,8 +901,14 @@ hipError_t launch_decode_walk(const char* state, int batch, int d, int r, int b_
                               const int32_t* pos, int s_exp, const double* r_prev, double* r_out,
                               hipStream_t st) {
   const int nstrip = (b_max + kStrip - 1) / kStrip;
-  hipLaunchKernelGGL(walk_row_strip_kernel, dim3((unsigned)batch, (unsigned)nstrip), dim3(kStripThreads), 0, st,
-                     state, batch, d, r, b_max, B, pos, s_exp, r_prev, r_out);
+  if (s_exp == 8)
+    hipLaunchKernelGGL(walk_row_strip_kernel<true>, dim3((unsigned)batch, (unsigned)nstrip),
+                       dim3(kStripThreads), 0, st, state, batch, d, r, b_max, B, pos, s_exp, r_prev,
+                       r_out);
+  else
+    hipLaunchKernelGGL(walk_row_strip_kernel<false>, dim3((unsigned)batch, (unsigned)nstrip),
+                       dim3(kStripThreads), 0, st, state, batch, d, r, b_max, B, pos, s_exp, r_prev,
+                       r_out);
   hipLaunchKernelGGL(walk_row_norm_kernel, dim3((unsigned)batch), dim3(256), 0, st, b_max, B, pos,
                      r_out);
   return hipGetLastError();
