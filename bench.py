@@ -420,6 +420,165 @@ def run_prefill(args, dev):
     return out, cpu_layer
 
 
+def run_speedup(args, dev) -> dict:
+    """Sparse vs dense at 16K-128K tokens (one layer of the Llama-3-8B
+    shape; the paper reports only such ratios, against FlashAttention).
+    Prefill: the whole sparse path (sketch, walk product, select, attention
+    at 20%) against dense causal attention, run by this library's kernel
+    with every block selected and by torch's flash SDPA when available.
+    Decode (batch 16, block 64): one step of the sparse path (KV append,
+    sketch, walk row, select, attention) against KV append + dense
+    attention over every cached token, both as captured HIP graphs."""
+    import torch
+    import synth
+    from paper_2602_07397_amd import binding as sw
+
+    lengths = [int(x) for x in args.speedup_lengths.split(",")]
+    stream = torch.cuda.current_stream(dev)
+
+    def timed(fn, reps):
+        fn()
+        torch.cuda.synchronize(dev)
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize(dev)
+        return e0.elapsed_time(e1) / reps
+
+    pre = []
+    base = synth.WORKLOADS["llama8b"]
+    for n in lengths:
+        w = synth.scaled(base, seqlens=(n,), layers=1)
+        cu = synth.cu_seqlens(w.seqlens)
+        B = w.B
+        signs, cols = synth.srht_params(w.d, w.r, w.seed)
+        ts, tc = torch.from_numpy(signs).to(dev), torch.from_numpy(cols).to(dev)
+        Q, K, V = synth.prefill_layer_inputs(w, 0, device=dev)
+        nb, nm, _ = sw.layout(cu, B)
+        f64 = dict(dtype=torch.float64, device=dev)
+        bufs = {"Qs": torch.empty((nb, w.r), **f64), "Ks": torch.empty((nb, w.r), **f64),
+                "A": torch.empty((nm,), **f64), "A_scale": torch.empty((1,), **f64)}
+        ws = torch.empty((sw.sketch_workspace_bytes(w.h_q, w.h_kv, w.d, cu, B),), dtype=torch.uint8,
+                         device=dev)
+        kmax = sw.select_max_count(cu, B, density_pct=w.pct)
+        kd = sw.select_max_count(cu, B, density_pct=100)
+        idx = torch.empty((nb, kmax), dtype=torch.int32, device=dev)
+        cnt = torch.empty((nb,), dtype=torch.int32, device=dev)
+        O = torch.empty_like(Q)
+        sk = sw.sketch_scores(Q, K, cu, B, ts, tc, out=bufs, workspace=ws)
+        R0 = sw.walk_update(sk["A"], sk["A_scale"], w.s, cu, B, None).clone()
+        Rb = torch.empty_like(R0)
+
+        def sparse_path():
+            s2 = sw.sketch_scores(Q, K, cu, B, ts, tc, out=bufs, workspace=ws)
+            R = sw.walk_update(s2["A"], s2["A_scale"], w.s, cu, B, R0, R_out=Rb)
+            sw.select_topk_blocks(R, cu, B, density_pct=w.pct, kmax=kmax, idx=idx, cnt=cnt)
+            sw.sparse_attn_prefill(Q, K, V, cu, B, idx, cnt, kmax, O=O)
+
+        reps = max(2, min(10, int(4e5 // n)))
+        t_path = timed(sparse_path, reps)
+        t_attn = timed(lambda: sw.sparse_attn_prefill(Q, K, V, cu, B, idx, cnt, kmax, O=O), reps)
+        idx_d, cnt_d, _ = sw.select_topk_blocks(R0, cu, B, density_pct=100, kmax=kd)
+        t_dense = timed(lambda: sw.sparse_attn_prefill(Q, K, V, cu, B, idx_d, cnt_d, kd, O=O), reps)
+        t_sdpa = None
+        try:
+            from torch.nn.attention import SDPBackend, sdpa_kernel
+            q4 = Q.unsqueeze(0)
+            k4 = K.repeat_interleave(w.h_q // w.h_kv, dim=0).unsqueeze(0)
+            v4 = V.repeat_interleave(w.h_q // w.h_kv, dim=0).unsqueeze(0)
+            with sdpa_kernel([SDPBackend.FLASH_ATTENTION]):
+                t_sdpa = timed(lambda: torch.nn.functional.scaled_dot_product_attention(
+                    q4, k4, v4, is_causal=True), reps)
+            del q4, k4, v4
+        except Exception as e:  # backend not built into this torch
+            print(f"[bench] flash SDPA unavailable: {type(e).__name__}: {e}", file=sys.stderr)
+        row = {"n": n, "sparse_path_ms": round(t_path, 3), "sparse_attention_ms": round(t_attn, 3),
+               "dense_ms_this_kernel": round(t_dense, 3),
+               "speedup_vs_dense_this_kernel": round(t_dense / t_path, 2)}
+        if t_sdpa is not None:
+            row["dense_ms_torch_flash_sdpa"] = round(t_sdpa, 3)
+            row["speedup_vs_torch_flash_sdpa"] = round(t_sdpa / t_path, 2)
+        pre.append(row)
+        print(f"[bench] speedup prefill {row}", file=sys.stderr, flush=True)
+        del Q, K, V, O, sk, bufs, ws, idx, cnt, idx_d, cnt_d, R0, Rb
+        torch.cuda.empty_cache()
+
+    dec = []
+    dbase = synth.WORKLOADS["decode"]
+    steps = 32
+    for n0 in lengths:
+        w = synth.scaled(dbase, kv_len=n0, layers=1)
+        batch, B = w.batch, w.B
+        T_max = n0 + steps + 1
+        b_max = -(-T_max // B)
+        signs, cols = synth.srht_params(w.d, w.r, w.seed)
+        ts, tc = torch.from_numpy(signs).to(dev), torch.from_numpy(cols).to(dev)
+        Kc = torch.empty((batch, w.h_kv, T_max, w.d), dtype=torch.bfloat16, device=dev)
+        Vc = torch.empty_like(Kc)
+        state = sw.new_decode_state(batch, w.d, w.r, b_max, dev)
+        for b in range(batch):
+            Qp, Kp, Vp = synth.decode_prefix_inputs(w, 0, b, device=dev)
+            skp = sw.sketch_scores(Qp, Kp, [0, n0], B, ts, tc, want_means=True)
+            sw.decode_state_init(state, batch, w.d, w.r, b_max, b, n0, B, skp)
+            Kc[b, :, :n0] = Kp
+            Vc[b, :, :n0] = Vp
+            del Qp, Kp, Vp, skp
+        q, kn, vn = synth.decode_step_inputs(w, 0, 0, device=dev)
+        pos = torch.full((batch,), n0, dtype=torch.int32, device=dev)
+        kmax = sw.select_max_count_decode(b_max, density_pct=w.pct)
+        idx = torch.empty((batch, kmax), dtype=torch.int32, device=dev)
+        cnt = torch.empty((batch,), dtype=torch.int32, device=dev)
+        r_prev = torch.ones((batch, b_max), dtype=torch.float64, device=dev)
+        r_out = torch.empty_like(r_prev)
+        o = torch.empty_like(q)
+        wsa = torch.empty((sw.decode_attn_workspace_bytes(batch, w.h_q, w.h_kv, w.d),), dtype=torch.uint8,
+                          device=dev)
+        bc = (n0 + steps) // B
+        idx_d = torch.arange(bc + 1, dtype=torch.int32, device=dev).repeat(batch, 1).contiguous()
+        cnt_d = torch.full((batch,), bc + 1, dtype=torch.int32, device=dev)
+
+        def sparse_step():
+            sw.kv_append(kn, vn, Kc, Vc, pos)
+            sw.sketch_scores_decode(q, kn, B, pos, ts, tc, b_max, state)
+            rr = sw.walk_update_decode(state, batch, w.d, w.r, b_max, B, pos, w.s, r_prev=r_prev,
+                                       r_out=r_out)
+            sw.select_topk_blocks_decode(rr, B, pos, density_pct=w.pct, kmax=kmax, idx=idx, cnt=cnt)
+            sw.sparse_attn_decode(q, Kc, Vc, B, pos, idx, cnt, kmax, O=o, workspace=wsa)
+            pos.add_(1)
+
+        def dense_step():
+            sw.kv_append(kn, vn, Kc, Vc, pos)
+            sw.sparse_attn_decode(q, Kc, Vc, B, pos, idx_d, cnt_d, bc + 1, O=o, workspace=wsa)
+            pos.add_(1)
+
+        res = {}
+        for name, fn in (("sparse", sparse_step), ("dense", dense_step)):
+            torch.cuda.synchronize(dev)
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                fn()
+            pos.fill_(n0)
+            torch.cuda.synchronize(dev)
+            res[name] = timed(g.replay, steps)
+            pos.fill_(n0)
+        row = {"kv_len": n0, "batch": batch, "sparse_step_us": round(res["sparse"] * 1e3, 1),
+               "dense_step_us": round(res["dense"] * 1e3, 1),
+               "speedup_vs_dense_this_kernel": round(res["dense"] / res["sparse"], 2)}
+        dec.append(row)
+        print(f"[bench] speedup decode {row}", file=sys.stderr, flush=True)
+        del Kc, Vc, state, idx_d
+        torch.cuda.empty_cache()
+    return {
+        "prefill_one_layer": pre,
+        "decode_one_layer": dec,
+        "note": "per layer of the Llama-3-8B shape (32 q / 8 kv heads, head_dim 128), density 20%; "
+                "the paper's ratios (against FlashAttention on an H100, whole model) are context only",
+    }
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -432,6 +591,9 @@ def main() -> int:
     ap.add_argument("--decode-steps", type=int, default=256)
     ap.add_argument("--decode-layers", type=int, default=None, help="override (debug only)")
     ap.add_argument("--decode-eager", action="store_true", help="launch the decode step eagerly")
+    ap.add_argument("--speedup", action="store_true",
+                    help="instead of the benchmark line, print sparse-vs-dense ratios at several lengths")
+    ap.add_argument("--speedup-lengths", default="16384,32768,65536,131072")
     ap.add_argument("--only", choices=("prefill", "decode", "copy"), default=None,
                     help="run one workload only (profiling); 'copy' runs the plain 1 GiB device "
                          "copy used to calibrate the FETCH_SIZE / WRITE_SIZE counters")
@@ -450,6 +612,9 @@ def main() -> int:
             dst.copy_(src)
         torch.cuda.synchronize(dev)
         print(json.dumps({"copy_bytes": 1 << 30, "copies": 5}), flush=True)
+        return 0
+    if args.speedup:
+        print(json.dumps({"speedup": run_speedup(args, dev)}), flush=True)
         return 0
     out = {}
     cpu_layer = None
