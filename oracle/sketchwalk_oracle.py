@@ -20,6 +20,8 @@ Sketch-and-Walk Sparse Attention for Efficient LLM Inference"):
   Sec. 2.2 estimate, Alg. 1 step 5                -> block_scores
   Sec. 2.3 walk, Alg. 1 step 6, lemma on walk
     accumulation across layers                    -> walk_weights, walk_step
+  walk transition variants (Sec. 1 and Fig. 2;
+    appendix lemma on stationary structure)       -> walk_weights_variant
   Alg. 1 step 7, Sec. 4.1 implementation details  -> row_budget, select_row,
                                                      select_blocks
   Alg. 1 step 8 (gather + softmax per head)       -> sparse_attention_prefill
@@ -37,6 +39,11 @@ design notes of the repository):
 * Causality: block scores above the diagonal (key block after query block)
   are zero in prefill, so the walk state stays lower triangular.
 * Walk power: element-wise integer power s >= 1, as Alg. 1 step 6 states.
+  Three other transitions are kept as variants (walk_weights_variant): the
+  power applied after clipping negative scores to zero; a causal row softmax
+  (the transition matrix of the appendix lemma on the walk's stationary
+  structure, with the sketched score rescaled to a block attention logit);
+  and the matrix power that the introduction's multi-hop walk describes.
 * Range: W is formed from A/c with c = max |A| of the layer, and every walk
   row is divided by its largest magnitude. Both rescale by positive factors
   and leave every row's ranking unchanged.
@@ -219,6 +226,66 @@ def walk_step(R_prev: Optional[np.ndarray], W: np.ndarray, normalize: bool = Tru
 
 
 # ---------------------------------------------------------------------------
+# Walk transition variants (readings of the walk step, see module header)
+# ---------------------------------------------------------------------------
+
+WALK_POWER = 0     # (A/c)^s element-wise: Alg. 1 step 6 as printed
+WALK_RELU = 1      # (max(A, 0)/c)^s element-wise
+WALK_SOFTMAX = 2   # causal row softmax of logit_scale * A (appendix lemma on
+                   # the walk's stationary structure, step 1)
+WALK_MATPOW = 3    # (A/c)^s as a matrix power: the s-hop walk inside one
+                   # layer that Sec. 1 and Fig. 2 describe
+
+
+def walk_weights_relu(A: np.ndarray, c: float, s: int) -> np.ndarray:
+    """Negative block scores clipped to zero before the element-wise power, so
+    that under even s a strongly negative score does not gain weight."""
+    return walk_weights(np.maximum(A, 0.0), c, s)
+
+
+def walk_weights_softmax(A: np.ndarray, logit_scale: float) -> np.ndarray:
+    """Row-stochastic transition matrix: row i is the softmax over the causal
+    key blocks j <= i of logit_scale * A[i, j]; entries above the diagonal are
+    zero. logit_scale = sqrt(r / d) turns the sketched score (which estimates
+    the block-mean inner product divided by sqrt(r)) into the block's mean
+    attention logit."""
+    b = A.shape[0]
+    W = np.zeros_like(A, dtype=np.float64)
+    for i in range(b):
+        z = logit_scale * A[i, :i + 1]
+        e = np.exp(z - np.max(z))
+        W[i, :i + 1] = e / e.sum()
+    return W
+
+
+def walk_weights_matpow(A: np.ndarray, c: float, s: int) -> np.ndarray:
+    """The s-th matrix power of A/c, by s - 1 successive products: entry
+    (i, j) sums the products of scores along every s-hop block path from i
+    to j."""
+    if int(s) != s or s < 1:
+        raise ValueError("s must be an integer >= 1")
+    X = A / c
+    W = X.copy()
+    for _ in range(int(s) - 1):
+        W = W @ X
+    return W
+
+
+def walk_weights_variant(variant: int, A: np.ndarray, c: float, s: int,
+                         logit_scale: float = 1.0) -> np.ndarray:
+    """W of one layer under the chosen transition (WALK_* constants)."""
+    if variant == WALK_POWER:
+        return walk_weights(A, c, s)
+    if variant == WALK_RELU:
+        return walk_weights_relu(A, c, s)
+    if variant == WALK_SOFTMAX:
+        return walk_weights_softmax(A, logit_scale)
+    if variant == WALK_MATPOW:
+        return walk_weights_matpow(A, c, s)
+    raise ValueError(f"unknown walk variant {variant}")
+
+
+# ---------------------------------------------------------------------------
 # Top-tau selection (Alg. 1 step 7; Sec. 4.1 implementation details)
 # ---------------------------------------------------------------------------
 
@@ -392,7 +459,7 @@ def decode_state_from_prefill(Q, K, B: int, signs, cols, b_max: int) -> DecodeLa
 
 def decode_layer_step(st: DecodeLayerState, q_new, k_new, p: int, r_prev: Optional[np.ndarray],
                       B: int, signs, cols, s: int, pct: int = 0, k: int = 0,
-                      flags: int = FORCE_BOTH):
+                      flags: int = FORCE_BOTH, variant: int = WALK_POWER):
     """Alg. 2 steps 2-6 for the token at 0-based position p of one sequence
     at one layer. q_new [h_q][d], k_new [h_kv][d]. Updates ``st`` in place and
     returns (walk row over key blocks 0..b_cur, selected blocks, gap)."""
@@ -423,7 +490,7 @@ def decode_layer_step(st: DecodeLayerState, q_new, k_new, p: int, r_prev: Option
     st.A[b_q, :b_cur + 1] = (Ks @ q_t) / math.sqrt(r)
     st.A[:b_q + 1, b_cur] = (Qs @ Ks[b_cur]) / math.sqrt(r)
     # step 5: walk, restricted to the row of the current query block
-    W = walk_weights(st.A[:b_cur + 1, :b_cur + 1], st.c, s)
+    W = walk_weights_variant(variant, st.A[:b_cur + 1, :b_cur + 1], st.c, s)
     row = W[b_q].copy() if r_prev is None else r_prev @ W
     m = float(np.max(np.abs(row)))
     if m > 0.0:
