@@ -57,6 +57,12 @@ extern "C" {
 #define SW_FORCE_FIRST 1u
 #define SW_FORCE_LAST 2u
 
+/* Walk transitions (sw_walk_update_variant, sw_walk_update_decode_variant). */
+#define SW_WALK_POWER 0   /* (A/c)^s element-wise: Alg. 1 step 6 */
+#define SW_WALK_RELU 1    /* (max(A, 0)/c)^s element-wise */
+#define SW_WALK_SOFTMAX 2 /* causal row softmax of logit_scale * A */
+#define SW_WALK_MATPOW 3  /* (A/c)^s as a matrix power */
+
 #define SW_MAX_SEQS 64          /* sequences per prefill call */
 #define SW_MAX_BLOCKS 4096      /* blocks per sequence */
 
@@ -130,6 +136,34 @@ int sw_sketch_scores(int dtype, const void* Q, const void* K, int h_q, int h_kv,
 int sw_walk_update(const double* A, const double* A_scale, int s,
                    int n_seqs, const int32_t* cu_seqlens /* [host] */, int B,
                    const double* R_prev, double* R_out, void* stream);
+
+/*
+ * sw_walk_update_variant - sw_walk_update with another transition in place
+ * of the element-wise power (the walk step of Sec. 2.3 under the readings
+ * that Sec. 1 / Fig. 2 and the appendix lemma on the walk's stationary
+ * structure suggest):
+ *   SW_WALK_POWER    W = (A/c)^s element-wise (identical to sw_walk_update);
+ *   SW_WALK_RELU     W = (max(A, 0)/c)^s element-wise: negative scores give
+ *                    zero weight instead of (-x)^s;
+ *   SW_WALK_SOFTMAX  W[i][j] = exp(t A[i][j]) / sum_{j' <= i} exp(t A[i][j'])
+ *                    for j <= i, 0 above the diagonal, t = logit_scale
+ *                    (sqrt(r / d) rescales the sketched score to a block
+ *                    attention logit); s is not used;
+ *   SW_WALK_MATPOW   W = (A/c)^s as a matrix power (entry (i, j) sums the
+ *                    score products along every s-hop block path), computed
+ *                    by binary exponentiation in fp64.
+ * Then R_out = W or R_prev W, rows divided by their largest magnitude, as in
+ * sw_walk_update. Arguments as there, plus:
+ * workspace: >= sw_walk_workspace_bytes(...) bytes of device memory, 8-byte
+ * aligned (may be NULL when that is 0); its contents are scratch.
+ * s in [1, 64] for every variant; logit_scale finite.
+ */
+int64_t sw_walk_workspace_bytes(int variant, int n_seqs, const int32_t* cu_seqlens /* [host] */,
+                                int B);
+int sw_walk_update_variant(int variant, const double* A, const double* A_scale, int s,
+                           double logit_scale, int n_seqs, const int32_t* cu_seqlens /* [host] */,
+                           int B, const double* R_prev, double* R_out, void* workspace,
+                           int64_t workspace_bytes, void* stream);
 
 /*
  * sw_select_topk_blocks - top-tau key blocks per query block: paper Alg. 1
@@ -241,6 +275,17 @@ int sw_sketch_scores_decode(int dtype, const void* q_new, const void* k_new, int
 int sw_walk_update_decode(const void* state, int batch, int d, int r, int b_max, int B,
                           const int32_t* pos, int s, const double* r_prev, double* r_out,
                           void* stream);
+
+/*
+ * sw_walk_update_decode_variant - sw_walk_update_decode with the transition
+ * chosen as in sw_walk_update_variant. SW_WALK_POWER and SW_WALK_RELU only:
+ * the other two need the whole weight matrix of every layer at every step
+ * (softmax normalizers of rows whose last column decode rewrites, or s
+ * matrix products) and return SW_ERR_UNSUPPORTED.
+ */
+int sw_walk_update_decode_variant(int variant, const void* state, int batch, int d, int r,
+                                  int b_max, int B, const int32_t* pos, int s,
+                                  const double* r_prev, double* r_out, void* stream);
 
 /* Host-only: the largest decode budget over rows of up to b_max blocks. */
 int sw_select_max_count_decode(int b_max, int k, int density_pct, uint32_t flags, int32_t* kmax);

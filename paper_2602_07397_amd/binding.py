@@ -24,6 +24,10 @@ SW_BF16 = 1
 FORCE_FIRST = 1
 FORCE_LAST = 2
 FORCE_BOTH = 3
+WALK_POWER = 0
+WALK_RELU = 1
+WALK_SOFTMAX = 2
+WALK_MATPOW = 3
 MAX_SEQS = 64
 MAX_BLOCKS = 4096
 
@@ -43,6 +47,9 @@ _SIGNATURES = {
     "sw_sketch_scores": (_c_int, [_c_int, _vp, _vp, _c_int, _c_int, _c_int, _c_int, _i32p, _c_int,
                                   _vp, _vp, _c_int, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _c_i64, _vp]),
     "sw_walk_update": (_c_int, [_vp, _vp, _c_int, _c_int, _i32p, _c_int, _vp, _vp, _vp]),
+    "sw_walk_workspace_bytes": (_c_i64, [_c_int, _c_int, _i32p, _c_int]),
+    "sw_walk_update_variant": (_c_int, [_c_int, _vp, _vp, _c_int, ctypes.c_double, _c_int, _i32p,
+                                        _c_int, _vp, _vp, _vp, _c_i64, _vp]),
     "sw_select_topk_blocks": (_c_int, [_vp, _c_int, _i32p, _c_int, _c_int, _c_int, ctypes.c_uint32,
                                        _vp, _vp, _c_int, _vp]),
     "sw_sparse_attn_prefill": (_c_int, [_c_int, _vp, _vp, _vp, _c_int, _c_int, _c_int, _c_int, _i32p,
@@ -55,6 +62,8 @@ _SIGNATURES = {
                                          _vp, _vp, _c_int, _c_int, _vp, _vp]),
     "sw_walk_update_decode": (_c_int, [_vp, _c_int, _c_int, _c_int, _c_int, _c_int, _vp, _c_int, _vp,
                                        _vp, _vp]),
+    "sw_walk_update_decode_variant": (_c_int, [_c_int, _vp, _c_int, _c_int, _c_int, _c_int, _c_int,
+                                               _vp, _c_int, _vp, _vp, _vp]),
     "sw_select_max_count_decode": (_c_int, [_c_int, _c_int, _c_int, ctypes.c_uint32, _i32p]),
     "sw_select_topk_blocks_decode": (_c_int, [_vp, _c_int, _c_int, _c_int, _vp, _c_int, _c_int,
                                               ctypes.c_uint32, _vp, _vp, _c_int, _vp]),
@@ -211,6 +220,36 @@ def walk_update(A: torch.Tensor, A_scale: torch.Tensor, s: int, cu_seqlens, B: i
     return R_out
 
 
+def walk_workspace_bytes(variant: int, cu_seqlens, B: int) -> int:
+    cu, n = _cu(cu_seqlens)
+    v = load().sw_walk_workspace_bytes(variant, n, cu, B)
+    if v < 0:
+        _check(1, "sw_walk_workspace_bytes")
+    return int(v)
+
+
+def walk_update_variant(variant: int, A: torch.Tensor, A_scale: torch.Tensor, s: int, cu_seqlens,
+                        B: int, R_prev: Optional[torch.Tensor] = None,
+                        R_out: Optional[torch.Tensor] = None, logit_scale: float = 1.0,
+                        workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """variant: WALK_POWER, WALK_RELU, WALK_SOFTMAX (uses ``logit_scale``,
+    not ``s``) or WALK_MATPOW."""
+    lib = load()
+    cu, n = _cu(cu_seqlens)
+    if R_out is None:
+        R_out = torch.empty_like(A)
+    wsb = walk_workspace_bytes(variant, cu_seqlens, B)
+    if wsb > 0 and (workspace is None or workspace.numel() < wsb):
+        workspace = torch.empty((wsb,), dtype=torch.uint8, device=A.device)
+    rc = lib.sw_walk_update_variant(
+        variant, _dev(A, "A", torch.float64), _dev(A_scale, "A_scale", torch.float64), s,
+        float(logit_scale), n, cu, B, _opt(R_prev, "R_prev", torch.float64),
+        _dev(R_out, "R_out", torch.float64), _opt(workspace, "workspace"),
+        0 if workspace is None else workspace.numel(), _stream(A.device))
+    _check(rc, "sw_walk_update_variant")
+    return R_out
+
+
 def select_topk_blocks(R: torch.Tensor, cu_seqlens, B: int, k: int = 0, density_pct: int = 20,
                        flags: int = FORCE_BOTH, kmax: Optional[int] = None,
                        idx: Optional[torch.Tensor] = None,
@@ -314,6 +353,22 @@ def walk_update_decode(state: torch.Tensor, batch: int, d: int, r: int, b_max: i
                                       _opt(r_prev, "r_prev", torch.float64),
                                       _dev(r_out, "r_out", torch.float64), _stream(dev))
     _check(rc, "sw_walk_update_decode")
+    return r_out
+
+
+def walk_update_decode_variant(variant: int, state: torch.Tensor, batch: int, d: int, r: int,
+                               b_max: int, B: int, pos: torch.Tensor, s: int,
+                               r_prev: Optional[torch.Tensor] = None,
+                               r_out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """variant: WALK_POWER or WALK_RELU (the others raise: unsupported)."""
+    dev = state.device
+    if r_out is None:
+        r_out = torch.empty((batch, b_max), dtype=torch.float64, device=dev)
+    rc = load().sw_walk_update_decode_variant(variant, _dev(state, "state", torch.uint8), batch, d,
+                                              r, b_max, B, _dev(pos, "pos", torch.int32), s,
+                                              _opt(r_prev, "r_prev", torch.float64),
+                                              _dev(r_out, "r_out", torch.float64), _stream(dev))
+    _check(rc, "sw_walk_update_decode_variant")
     return r_out
 
 

@@ -203,10 +203,22 @@ int sw_sketch_scores(int dtype, const void* Q, const void* K, int h_q, int h_kv,
   return hip_status(e, "sw_sketch_scores launch");
 }
 
-int sw_walk_update(const double* A, const double* A_scale, int s, int n_seqs,
-                   const int32_t* cu_seqlens, int B, const double* R_prev, double* R_out,
-                   void* stream) {
+int64_t sw_walk_workspace_bytes(int variant, int n_seqs, const int32_t* cu_seqlens, int B) {
+  if (variant < SW_WALK_POWER || variant > SW_WALK_MATPOW) return -1;
+  sw::SeqMeta m;
+  int64_t nb = 0, nm = 0;
+  if (build_meta(n_seqs, cu_seqlens, B, &m, &nb, &nm) != SW_OK) return -1;
+  return sw::walk_workspace_bytes(variant, nm);
+}
+
+int sw_walk_update_variant(int variant, const double* A, const double* A_scale, int s,
+                           double logit_scale, int n_seqs, const int32_t* cu_seqlens, int B,
+                           const double* R_prev, double* R_out, void* workspace,
+                           int64_t workspace_bytes, void* stream) {
+  if (variant < SW_WALK_POWER || variant > SW_WALK_MATPOW)
+    return fail(SW_ERR_INVALID_ARG, "unknown walk variant %d", variant);
   if (s < 1 || s > 64) return fail(SW_ERR_INVALID_ARG, "s=%d outside [1, 64]", s);
+  if (!isfinite(logit_scale)) return fail(SW_ERR_INVALID_ARG, "logit_scale is not finite");
   sw::SeqMeta m;
   int64_t nb = 0, nm = 0;
   CHECK(build_meta(n_seqs, cu_seqlens, B, &m, &nb, &nm));
@@ -215,9 +227,24 @@ int sw_walk_update(const double* A, const double* A_scale, int s, int n_seqs,
   CHECK(check_ptr(R_out, 8, "R_out"));
   if (R_prev && !aligned(R_prev, 8)) return fail(SW_ERR_INVALID_ARG, "R_prev misaligned");
   if (R_out == R_prev || R_out == A) return fail(SW_ERR_INVALID_ARG, "R_out aliases an input");
-  hipError_t e = sw::launch_walk(A, A_scale, s, m, nb, R_prev, R_out,
+  const int64_t need = sw::walk_workspace_bytes(variant, nm);
+  if (need > 0) {
+    CHECK(check_ptr(workspace, 8, "workspace"));
+    if (workspace_bytes < need)
+      return fail(SW_ERR_INVALID_ARG, "workspace_bytes=%lld < required %lld",
+                  (long long)workspace_bytes, (long long)need);
+  }
+  hipError_t e = sw::launch_walk(variant, A, A_scale, s, logit_scale, m, nb, R_prev, R_out,
+                                 static_cast<double*>(workspace),
                                  reinterpret_cast<hipStream_t>(stream));
   return hip_status(e, "sw_walk_update launch");
+}
+
+int sw_walk_update(const double* A, const double* A_scale, int s, int n_seqs,
+                   const int32_t* cu_seqlens, int B, const double* R_prev, double* R_out,
+                   void* stream) {
+  return sw_walk_update_variant(SW_WALK_POWER, A, A_scale, s, 1.0, n_seqs, cu_seqlens, B, R_prev,
+                                R_out, nullptr, 0, stream);
 }
 
 int sw_select_topk_blocks(const double* R, int n_seqs, const int32_t* cu_seqlens, int B, int k,
@@ -351,9 +378,13 @@ int sw_sketch_scores_decode(int dtype, const void* q_new, const void* k_new, int
   return hip_status(e, "sw_sketch_scores_decode launch");
 }
 
-int sw_walk_update_decode(const void* state, int batch, int d, int r, int b_max, int B,
-                          const int32_t* pos, int s, const double* r_prev, double* r_out,
-                          void* stream) {
+int sw_walk_update_decode_variant(int variant, const void* state, int batch, int d, int r,
+                                  int b_max, int B, const int32_t* pos, int s,
+                                  const double* r_prev, double* r_out, void* stream) {
+  if (variant == SW_WALK_SOFTMAX || variant == SW_WALK_MATPOW)
+    return fail(SW_ERR_UNSUPPORTED, "walk variant %d is not available in decode", variant);
+  if (variant != SW_WALK_POWER && variant != SW_WALK_RELU)
+    return fail(SW_ERR_INVALID_ARG, "unknown walk variant %d", variant);
   if (s < 1 || s > 64) return fail(SW_ERR_INVALID_ARG, "s=%d outside [1, 64]", s);
   CHECK(check_decode_shape(batch, d, r, b_max, B));
   CHECK(check_ptr(state, 256, "state"));
@@ -362,8 +393,16 @@ int sw_walk_update_decode(const void* state, int batch, int d, int r, int b_max,
   if (r_prev && !aligned(r_prev, 8)) return fail(SW_ERR_INVALID_ARG, "r_prev misaligned");
   if (r_prev == r_out) return fail(SW_ERR_INVALID_ARG, "r_out aliases r_prev");
   hipError_t e = sw::launch_decode_walk(reinterpret_cast<const char*>(state), batch, d, r, b_max, B,
-                                        pos, s, r_prev, r_out, reinterpret_cast<hipStream_t>(stream));
+                                        pos, s, variant == SW_WALK_RELU, r_prev, r_out,
+                                        reinterpret_cast<hipStream_t>(stream));
   return hip_status(e, "sw_walk_update_decode launch");
+}
+
+int sw_walk_update_decode(const void* state, int batch, int d, int r, int b_max, int B,
+                          const int32_t* pos, int s, const double* r_prev, double* r_out,
+                          void* stream) {
+  return sw_walk_update_decode_variant(SW_WALK_POWER, state, batch, d, r, b_max, B, pos, s, r_prev,
+                                       r_out, stream);
 }
 
 int sw_select_max_count_decode(int b_max, int k, int density_pct, uint32_t flags, int32_t* kmax) {

@@ -277,7 +277,9 @@ constexpr int kStrip = 32;               // columns per workgroup (8 lanes x 4)
 constexpr int kRowGroups = SW_STRIP_RG;  // row groups per workgroup
 constexpr int kStripThreads = 8 * kRowGroups;
 
-template <bool S8>   // S8: s = 8, the paper's exponent (three squarings, no loop)
+// S8: s = 8, the paper's exponent (three squarings, no loop). RELU: negative
+// scores are clipped to zero before the power.
+template <bool S8, bool RELU>
 __global__ __launch_bounds__(kStripThreads) void walk_row_strip_kernel(const char* __restrict__ state,
                                                              int batch, int d, int r, int b_max,
                                                              int B, const int32_t* __restrict__ pos,
@@ -297,6 +299,7 @@ __global__ __launch_bounds__(kStripThreads) void walk_row_strip_kernel(const cha
   const int col0 = reinterpret_cast<const int32_t*>(state + L.col0)[bi];
   const float* A = reinterpret_cast<const float*>(state + L.a) + (long long)bi * b_max * L.lda;
   auto pw = [&](double x) {
+    if constexpr (RELU) x = fmax(x, 0.0);
     if constexpr (S8) {
       const double x2 = x * x, x4 = x2 * x2;
       return x4 * x4;
@@ -898,17 +901,22 @@ hipError_t launch_decode_sketch(int dtype, const void* q_new, const void* k_new,
 }
 
 hipError_t launch_decode_walk(const char* state, int batch, int d, int r, int b_max, int B,
-                              const int32_t* pos, int s_exp, const double* r_prev, double* r_out,
-                              hipStream_t st) {
+                              const int32_t* pos, int s_exp, bool relu, const double* r_prev,
+                              double* r_out, hipStream_t st) {
   const int nstrip = (b_max + kStrip - 1) / kStrip;
-  if (s_exp == 8)
-    hipLaunchKernelGGL(walk_row_strip_kernel<true>, dim3((unsigned)batch, (unsigned)nstrip),
-                       dim3(kStripThreads), 0, st, state, batch, d, r, b_max, B, pos, s_exp, r_prev,
-                       r_out);
+  const dim3 grid((unsigned)batch, (unsigned)nstrip), blk(kStripThreads);
+  if (s_exp == 8 && !relu)
+    hipLaunchKernelGGL((walk_row_strip_kernel<true, false>), grid, blk, 0, st, state, batch, d, r,
+                       b_max, B, pos, s_exp, r_prev, r_out);
+  else if (s_exp == 8)
+    hipLaunchKernelGGL((walk_row_strip_kernel<true, true>), grid, blk, 0, st, state, batch, d, r,
+                       b_max, B, pos, s_exp, r_prev, r_out);
+  else if (!relu)
+    hipLaunchKernelGGL((walk_row_strip_kernel<false, false>), grid, blk, 0, st, state, batch, d, r,
+                       b_max, B, pos, s_exp, r_prev, r_out);
   else
-    hipLaunchKernelGGL(walk_row_strip_kernel<false>, dim3((unsigned)batch, (unsigned)nstrip),
-                       dim3(kStripThreads), 0, st, state, batch, d, r, b_max, B, pos, s_exp, r_prev,
-                       r_out);
+    hipLaunchKernelGGL((walk_row_strip_kernel<false, true>), grid, blk, 0, st, state, batch, d, r,
+                       b_max, B, pos, s_exp, r_prev, r_out);
   hipLaunchKernelGGL(walk_row_norm_kernel, dim3((unsigned)batch), dim3(256), 0, st, b_max, B, pos,
                      r_out);
   return hipGetLastError();

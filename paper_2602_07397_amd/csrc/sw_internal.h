@@ -48,8 +48,11 @@ hipError_t launch_sketch(int dtype, const void* Q, const void* K, int h_q, int h
                          const int32_t* cols, int r, double* Qs, double* Ks, double* A,
                          double* A_scale, double* Qbar, double* Kbar, void* ws, hipStream_t st);
 
-hipError_t launch_walk(const double* A, const double* A_scale, int s_exp, const SeqMeta& meta,
-                       int64_t nb, const double* R_prev, double* R_out, hipStream_t st);
+int64_t walk_workspace_bytes(int variant, int64_t nm);
+
+hipError_t launch_walk(int variant, const double* A, const double* A_scale, int s_exp,
+                       double logit_scale, const SeqMeta& meta, int64_t nb, const double* R_prev,
+                       double* R_out, double* ws, hipStream_t st);
 
 hipError_t launch_select(const double* R, const SeqMeta& meta, int64_t nb, int k, int pct,
                          uint32_t flags, int32_t* idx, int32_t* cnt, int kmax, hipStream_t st);
@@ -74,8 +77,8 @@ hipError_t launch_decode_sketch(int dtype, const void* q_new, const void* k_new,
                                 hipStream_t st);
 
 hipError_t launch_decode_walk(const char* state, int batch, int d, int r, int b_max, int B,
-                              const int32_t* pos, int s_exp, const double* r_prev, double* r_out,
-                              hipStream_t st);
+                              const int32_t* pos, int s_exp, bool relu, const double* r_prev,
+                              double* r_out, hipStream_t st);
 
 hipError_t launch_select_decode(const double* rows, int batch, int b_max, int B,
                                 const int32_t* pos, int k, int pct, uint32_t flags, int32_t* idx,

@@ -1,13 +1,20 @@
 // Sketch-Determined Walk kernels (paper Sec. 2.3, Alg. 1 step 6).
 //
-//  walk_first_kernel  first walked layer: R = (A/c)^s, row-normalised.
-//  walk_gemm_kernel   R = R_prev (A/c)^s. One wavefront per 16x16 output
-//                     tile on fp64 MFMA 16x16x4; the element-wise power is
-//                     taken while loading the B operand; tiles above the
-//                     diagonal are written as zeros and the k-range of a tile
-//                     is clipped to [j0, i_max] (both factors are lower
-//                     triangular).
-//  walk_norm_kernel   divides each row by its largest magnitude.
+//  walk_first_kernel    first walked layer: R = W(A), row-normalised.
+//  walk_gemm_kernel     C = X W(Y) for lower triangular X, Y. One wavefront per
+//                       16x16 output tile on fp64 MFMA 16x16x4; the weight
+//                       transform W is applied while loading the B operand;
+//                       tiles above the diagonal are written as zeros and the
+//                       k-range of a tile is clipped to [j0, i_max].
+//  walk_softmax_kernel  causal row softmax of t*A (the transition matrix of
+//                       the appendix lemma on the walk's stationary structure).
+//  walk_norm_kernel     divides each row by its largest magnitude.
+//
+// Weight transforms (template parameter): the element-wise power (A/c)^s of
+// Alg. 1 step 6, the same power after clipping negative scores to zero, or
+// the identity (the operand already holds weights). The matrix-power variant
+// (the within-layer multi-hop walk of Sec. 1 and Fig. 2) is built from
+// walk_gemm_kernel by binary exponentiation.
 #include "sw_common.h"
 #include "sw_internal.h"
 
@@ -29,6 +36,15 @@ __device__ __forceinline__ double pow_int(double x, int s) {
   return r;
 }
 
+enum WeightFn { kWPow = 0, kWRelu = 1, kWIdent = 2 };
+
+template <int F>
+__device__ __forceinline__ double weight_of(double a, double inv_c, int s) {
+  if constexpr (F == kWPow) return pow_int(a * inv_c, s);
+  if constexpr (F == kWRelu) return pow_int(fmax(a, 0.0) * inv_c, s);
+  return a;
+}
+
 __device__ __forceinline__ double scale_of(const double* A_scale, int s) {
   const double c = A_scale[s];
   return c > 0.0 ? c : 1.0;
@@ -43,6 +59,17 @@ __device__ __forceinline__ double block_max_256(double v, double* tmp) {
   return v;
 }
 
+__device__ __forceinline__ double block_sum_256(double v, double* tmp) {
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+  if ((threadIdx.x & 63) == 0) tmp[threadIdx.x >> 6] = v;
+  __syncthreads();
+  v = (tmp[0] + tmp[1]) + (tmp[2] + tmp[3]);
+  __syncthreads();
+  return v;
+}
+
+// NORM = false writes W(A) itself (the factor of a matrix power).
+template <int F, bool NORM = true>
 __global__ __launch_bounds__(256) void walk_first_kernel(const double* __restrict__ A,
                                                          const double* __restrict__ A_scale,
                                                          int s_exp, SeqMeta m,
@@ -52,15 +79,16 @@ __global__ __launch_bounds__(256) void walk_first_kernel(const double* __restric
   const int s = seq_of_block(m, row);
   const int i = row - m.blk_start[s];
   const int b = m.blk_start[s + 1] - m.blk_start[s];
-  const double inv_c = 1.0 / scale_of(A_scale, s);
+  const double inv_c = F == kWIdent ? 1.0 : 1.0 / scale_of(A_scale, s);
   const double* Ar = A + m.mat_start[s] + (long long)i * b;
   double* Rr = R + m.mat_start[s] + (long long)i * b;
   double mx = 0.0;
   for (int j = threadIdx.x; j < b; j += 256) {
-    const double w = (j <= i) ? pow_int(Ar[j] * inv_c, s_exp) : 0.0;
+    const double w = (j <= i) ? weight_of<F>(Ar[j], inv_c, s_exp) : 0.0;
     Rr[j] = w;
     mx = fmax(mx, fabs(w));
   }
+  if (!NORM) return;
   mx = block_max_256(mx, tmp);
   if (mx > 0.0) {
     const double inv = 1.0 / mx;
@@ -68,6 +96,7 @@ __global__ __launch_bounds__(256) void walk_first_kernel(const double* __restric
   }
 }
 
+template <int F>
 __global__ __launch_bounds__(256) void walk_gemm_kernel(const double* __restrict__ A,
                                                         const double* __restrict__ A_scale,
                                                         int s_exp, SeqMeta m, int total_tiles,
@@ -93,7 +122,7 @@ __global__ __launch_bounds__(256) void walk_gemm_kernel(const double* __restrict
     }
     return;
   }
-  const double inv_c = 1.0 / scale_of(A_scale, s);
+  const double inv_c = F == kWIdent ? 1.0 : 1.0 / scale_of(A_scale, s);
   const int ra = ti * 16 + (l & 15);   // A-operand row (output row)
   const int cb = tj * 16 + (l & 15);   // B-operand column (output column)
   const int kend = min(ti * 16 + 15, b - 1);
@@ -101,13 +130,40 @@ __global__ __launch_bounds__(256) void walk_gemm_kernel(const double* __restrict
   for (int k0 = (tj * 16) & ~3; k0 <= kend; k0 += 4) {
     const int k = k0 + (l >> 4);
     const double av = (ra < b && k <= ra) ? Ps[(long long)ra * b + k] : 0.0;
-    const double bv = (k < b && cb <= k) ? pow_int(As[(long long)k * b + cb] * inv_c, s_exp) : 0.0;
+    const double bv = (k < b && cb <= k) ? weight_of<F>(As[(long long)k * b + cb], inv_c, s_exp) : 0.0;
     acc = __builtin_amdgcn_mfma_f64_16x16x4f64(av, bv, acc, 0, 0, 0);
   }
   for (int v = 0; v < 4; ++v) {
     const int ri = ti * 16 + (l >> 4) + 4 * v, cj = tj * 16 + (l & 15);
     if (ri < b && cj < b) Rs[(long long)ri * b + cj] = (cj <= ri) ? acc[v] : 0.0;
   }
+}
+
+// Row i of W: exp(t A[i,j] - max) / sum over the causal blocks j <= i; zeros
+// above the diagonal. The exponentials are stored, then scaled by 1/sum by
+// the same thread that wrote them.
+__global__ __launch_bounds__(256) void walk_softmax_kernel(const double* __restrict__ A,
+                                                           double t, SeqMeta m,
+                                                           double* __restrict__ W) {
+  __shared__ double tmp[4];
+  const int row = blockIdx.x;
+  const int s = seq_of_block(m, row);
+  const int i = row - m.blk_start[s];
+  const int b = m.blk_start[s + 1] - m.blk_start[s];
+  const double* Ar = A + m.mat_start[s] + (long long)i * b;
+  double* Wr = W + m.mat_start[s] + (long long)i * b;
+  double mx = -INFINITY;
+  for (int j = threadIdx.x; j <= i; j += 256) mx = fmax(mx, t * Ar[j]);
+  mx = block_max_256(mx, tmp);
+  double sum = 0.0;
+  for (int j = threadIdx.x; j < b; j += 256) {
+    const double e = (j <= i) ? exp(t * Ar[j] - mx) : 0.0;
+    Wr[j] = e;
+    sum += e;
+  }
+  sum = block_sum_256(sum, tmp);
+  const double inv = 1.0 / sum;
+  for (int j = threadIdx.x; j <= i; j += 256) Wr[j] = Wr[j] * inv;
 }
 
 __global__ __launch_bounds__(256) void walk_norm_kernel(SeqMeta m, double* __restrict__ R) {
@@ -126,25 +182,101 @@ __global__ __launch_bounds__(256) void walk_norm_kernel(SeqMeta m, double* __res
   }
 }
 
-hipError_t launch_walk(const double* A, const double* A_scale, int s_exp, const SeqMeta& meta,
-                       int64_t nb, const double* R_prev, double* R_out, hipStream_t st) {
-  if (R_prev == nullptr) {
-    hipLaunchKernelGGL(walk_first_kernel, dim3((unsigned)nb), dim3(256), 0, st, A, A_scale, s_exp,
-                       meta, R_out);
-    return hipGetLastError();
-  }
-  SeqMeta m2 = meta;
+namespace {
+
+int gemm_tiles(const SeqMeta& meta, SeqMeta* m2) {
+  *m2 = meta;
   int total = 0;
   for (int s = 0; s < meta.n_seqs; ++s) {
-    m2.aux_start[s] = total;
+    m2->aux_start[s] = total;
     const int b = meta.blk_start[s + 1] - meta.blk_start[s];
     const int tb = (b + 15) / 16;
     total += tb * tb;
   }
-  m2.aux_start[meta.n_seqs] = total;
-  hipLaunchKernelGGL(walk_gemm_kernel, dim3((unsigned)((total + 3) / 4)), dim3(256), 0, st, A,
-                     A_scale, s_exp, m2, total, R_prev, R_out);
-  hipLaunchKernelGGL(walk_norm_kernel, dim3((unsigned)nb), dim3(256), 0, st, meta, R_out);
+  m2->aux_start[meta.n_seqs] = total;
+  return total;
+}
+
+// C = X W(Y): X, Y, C lower triangular per sequence; C covers every entry.
+template <int F>
+void gemm(const double* X, const double* Y, const double* A_scale, int s_exp, const SeqMeta& m2,
+          int total, double* C, hipStream_t st) {
+  hipLaunchKernelGGL(walk_gemm_kernel<F>, dim3((unsigned)((total + 3) / 4)), dim3(256), 0, st, Y,
+                     A_scale, s_exp, m2, total, X, C);
+}
+
+}  // namespace
+
+int64_t walk_workspace_bytes(int variant, int64_t nm) {
+  if (variant == SW_WALK_SOFTMAX) return 8 * nm;
+  if (variant == SW_WALK_MATPOW) return 16 * nm;
+  return 0;
+}
+
+hipError_t launch_walk(int variant, const double* A, const double* A_scale, int s_exp,
+                       double logit_scale, const SeqMeta& meta, int64_t nb, const double* R_prev,
+                       double* R_out, double* ws, hipStream_t st) {
+  const dim3 rows((unsigned)nb), blk(256);
+  SeqMeta m2;
+  const int total = gemm_tiles(meta, &m2);
+  if (variant == SW_WALK_MATPOW && s_exp == 1) variant = SW_WALK_POWER;  // X^1 = X
+  switch (variant) {
+    case SW_WALK_POWER:
+    case SW_WALK_RELU:
+      if (R_prev == nullptr) {
+        if (variant == SW_WALK_POWER)
+          hipLaunchKernelGGL(walk_first_kernel<kWPow>, rows, blk, 0, st, A, A_scale, s_exp, meta,
+                             R_out);
+        else
+          hipLaunchKernelGGL(walk_first_kernel<kWRelu>, rows, blk, 0, st, A, A_scale, s_exp, meta,
+                             R_out);
+        return hipGetLastError();
+      }
+      if (variant == SW_WALK_POWER)
+        gemm<kWPow>(R_prev, A, A_scale, s_exp, m2, total, R_out, st);
+      else
+        gemm<kWRelu>(R_prev, A, A_scale, s_exp, m2, total, R_out, st);
+      break;
+    case SW_WALK_SOFTMAX: {
+      double* W = R_prev == nullptr ? R_out : ws;
+      hipLaunchKernelGGL(walk_softmax_kernel, rows, blk, 0, st, A, logit_scale, meta, W);
+      if (R_prev != nullptr) gemm<kWIdent>(R_prev, W, nullptr, 1, m2, total, R_out, st);
+      break;
+    }
+    case SW_WALK_MATPOW: {
+      // Left-to-right binary exponentiation of X = A/c: square for every bit
+      // below the leading one, multiply by X (read from A through the s = 1
+      // power) where the bit is set. Two ping-pong buffers; without R_prev
+      // the last product is written to R_out directly.
+      const int64_t nm = meta.mat_start[meta.n_seqs];
+      double* buf[2] = {ws, ws + nm};
+      const int top = 31 - __builtin_clz((unsigned)s_exp);
+      int nprod = 0;
+      for (int bit = top - 1; bit >= 0; --bit) nprod += 1 + ((s_exp >> bit) & 1);
+      hipLaunchKernelGGL((walk_first_kernel<kWPow, false>), rows, blk, 0, st, A, A_scale, 1, meta,
+                         buf[0]);
+      const double* cur = buf[0];
+      int ci = 0, k = 0;
+      for (int bit = top - 1; bit >= 0; --bit) {
+        const int steps = 1 + ((s_exp >> bit) & 1);
+        for (int step = 0; step < steps; ++step) {
+          const bool last = ++k == nprod;
+          double* dst = (last && R_prev == nullptr) ? R_out : buf[1 - ci];
+          if (step == 0)
+            gemm<kWIdent>(cur, cur, nullptr, 1, m2, total, dst, st);
+          else
+            gemm<kWPow>(cur, A, A_scale, 1, m2, total, dst, st);
+          cur = dst;
+          ci = 1 - ci;
+        }
+      }
+      if (R_prev != nullptr) gemm<kWIdent>(R_prev, cur, nullptr, 1, m2, total, R_out, st);
+      break;
+    }
+    default:
+      return hipErrorInvalidValue;
+  }
+  hipLaunchKernelGGL(walk_norm_kernel, rows, blk, 0, st, meta, R_out);
   return hipGetLastError();
 }
 

@@ -19,8 +19,9 @@ U = pytest.importorskip("_gpu_util")
 class DecodeRun:
     """Runs the same decode on the GPU (through the C ABI) and on the oracle."""
 
-    def __init__(self, w, prompts, steps, T_extra=0):
+    def __init__(self, w, prompts, steps, T_extra=0, variant=sw.WALK_POWER):
         self.w = w
+        self.variant = variant
         self.B = w.B
         self.d = w.d
         self.r = w.r
@@ -68,8 +69,12 @@ class DecodeRun:
             qd, kd, vd = U.to_dev(q), U.to_dev(kk), U.to_dev(v)
             sw.kv_append(kd, vd, self.Kc[l], self.Vc[l], pos)
             sw.sketch_scores_decode(qd, kd, self.B, pos, self.ts, self.tc, self.b_max, self.state[l])
-            r_gpu = sw.walk_update_decode(self.state[l], self.batch, w.d, w.r, self.b_max, self.B, pos,
-                                          w.s, r_prev=r_gpu)
+            if self.variant == sw.WALK_POWER:
+                r_gpu = sw.walk_update_decode(self.state[l], self.batch, w.d, w.r, self.b_max, self.B,
+                                              pos, w.s, r_prev=r_gpu)
+            else:
+                r_gpu = sw.walk_update_decode_variant(self.variant, self.state[l], self.batch, w.d,
+                                                      w.r, self.b_max, self.B, pos, w.s, r_prev=r_gpu)
             idx, cnt, _ = sw.select_topk_blocks_decode(r_gpu, self.B, pos, density_pct=w.pct,
                                                        kmax=self.kmax)
             out = sw.sparse_attn_decode(qd, self.Kc[l], self.Vc[l], self.B, pos, idx, cnt, self.kmax)
@@ -85,7 +90,8 @@ class DecodeRun:
                 self.Kh[l][b][:, p] = kh[b]
                 self.Vh[l][b][:, p] = vh[b]
                 row, sel, gap = O.decode_layer_step(self.ost[l][b], qh[b], kh[b], p, r_ref[b], self.B,
-                                                    self.signs, self.cols, w.s, pct=w.pct)
+                                                    self.signs, self.cols, w.s, pct=w.pct,
+                                                    variant=self.variant)
                 r_ref[b] = row
                 stats["werr"] = max(stats["werr"], U.max_abs(rg[b, :bc + 1], row))
                 assert np.all(rg[b, bc + 1:] == 0.0)
