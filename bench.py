@@ -18,6 +18,7 @@ from __future__ import annotations
 
 import argparse
 import json
+import math
 import os
 import sys
 import time
@@ -579,6 +580,81 @@ def run_speedup(args, dev) -> dict:
     }
 
 
+def run_walk_variants(args, dev) -> dict:
+    """Walk transition variants at the Llama-3-8B shape (one layer, block
+    128) for each prompt length in --speedup-lengths: time of one walk update
+    with a previous walk state (the per-layer call after the first layer),
+    the fp64 MFMA rate of its block products, and how much of the default
+    variant's selection at 20% each variant keeps."""
+    import torch
+    import synth
+    from paper_2602_07397_amd import binding as sw
+
+    names = {sw.WALK_POWER: "power", sw.WALK_RELU: "relu_power", sw.WALK_SOFTMAX: "row_softmax",
+             sw.WALK_MATPOW: "matrix_power"}
+    stream = torch.cuda.current_stream(dev)
+    base = synth.WORKLOADS["llama8b"]
+    rows = []
+    for n in [int(x) for x in args.speedup_lengths.split(",")]:
+        w = synth.scaled(base, seqlens=(n,), layers=2)
+        cu = synth.cu_seqlens(w.seqlens)
+        B = w.B
+        signs, cols = synth.srht_params(w.d, w.r, w.seed)
+        ts, tc = torch.from_numpy(signs).to(dev), torch.from_numpy(cols).to(dev)
+        sks = []
+        for layer in range(2):
+            Q, K, _ = synth.prefill_layer_inputs(w, layer, device=dev)
+            sks.append(sw.sketch_scores(Q, K, cu, B, ts, tc))
+            del Q, K
+        b = -(-n // B)
+        macs = b * (b + 1) * (b + 2) // 6          # one lower x lower triangular product
+        t = math.sqrt(w.r / w.d)
+        kmax = sw.select_max_count(cu, B, density_pct=w.pct)
+        base_sel = None
+        for v in (sw.WALK_POWER, sw.WALK_RELU, sw.WALK_SOFTMAX, sw.WALK_MATPOW):
+            R0 = sw.walk_update_variant(v, sks[0]["A"], sks[0]["A_scale"], w.s, cu, B, logit_scale=t)
+            R1 = torch.empty_like(R0)
+            wsb = sw.walk_workspace_bytes(v, cu, B)
+            ws = torch.empty((max(wsb, 256),), dtype=torch.uint8, device=dev)
+
+            def step():
+                sw.walk_update_variant(v, sks[1]["A"], sks[1]["A_scale"], w.s, cu, B, R0, R1,
+                                       logit_scale=t, workspace=ws)
+
+            step()
+            torch.cuda.synchronize(dev)
+            reps = 50
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(reps):
+                step()
+            e1.record(stream)
+            torch.cuda.synchronize(dev)
+            ms = e0.elapsed_time(e1) / reps
+            if v == sw.WALK_MATPOW:
+                top = w.s.bit_length() - 1
+                nprod = sum(1 + ((w.s >> bit) & 1) for bit in range(top - 1, -1, -1)) + 1
+            else:
+                nprod = 1
+            idx, cnt, _ = sw.select_topk_blocks(R1, cu, B, density_pct=w.pct, kmax=kmax)
+            sel = [set(r[:c].tolist()) for r, c in zip(idx.cpu().numpy(), cnt.cpu().numpy())]
+            if base_sel is None:
+                base_sel = sel
+            kept = sum(len(a & b_) for a, b_ in zip(sel, base_sel)) / sum(len(a) for a in base_sel)
+            rows.append({"n": n, "blocks": b, "variant": names[v], "ms": round(ms, 4),
+                         "block_products": nprod,
+                         "fp64_tflops": round(2.0 * macs * nprod / (ms * 1e-3) / 1e12, 2),
+                         "kept_of_power_selection": round(kept, 4)})
+            print(f"[bench] walk {names[v]} n={n}: {ms:.4f} ms", file=sys.stderr, flush=True)
+        del sks
+        torch.cuda.empty_cache()
+    return {"rows": rows, "s": base.s, "density_pct": base.pct, "block": base.B,
+            "fp64_mfma_peak_tflops": 78.6,
+            "note": "one walk update with a previous state (second layer); the softmax variant "
+                    "uses logit scale sqrt(r/d)"}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -594,6 +670,9 @@ def main() -> int:
     ap.add_argument("--speedup", action="store_true",
                     help="instead of the benchmark line, print sparse-vs-dense ratios at several lengths")
     ap.add_argument("--speedup-lengths", default="16384,32768,65536,131072")
+    ap.add_argument("--walk-variants", action="store_true",
+                    help="instead of the benchmark line, time the walk transition variants at the "
+                         "--speedup-lengths")
     ap.add_argument("--only", choices=("prefill", "decode", "copy"), default=None,
                     help="run one workload only (profiling); 'copy' runs the plain 1 GiB device "
                          "copy used to calibrate the FETCH_SIZE / WRITE_SIZE counters")
@@ -615,6 +694,9 @@ def main() -> int:
         return 0
     if args.speedup:
         print(json.dumps({"speedup": run_speedup(args, dev)}), flush=True)
+        return 0
+    if args.walk_variants:
+        print(json.dumps({"walk_variants": run_walk_variants(args, dev)}), flush=True)
         return 0
     out = {}
     cpu_layer = None

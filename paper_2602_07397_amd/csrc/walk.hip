@@ -2,13 +2,15 @@
 //
 //  walk_first_kernel    first walked layer: R = W(A), row-normalised.
 //  walk_gemm_kernel     C = X W(Y) for lower triangular X, Y. One wavefront per
-//                       16x16 output tile on fp64 MFMA 16x16x4; the weight
-//                       transform W is applied while loading the B operand;
-//                       tiles above the diagonal are written as zeros and the
-//                       k-range of a tile is clipped to [j0, i_max].
+//                       16x16 output tile on or below the diagonal, on fp64
+//                       MFMA 16x16x4; the weight transform W is applied to the
+//                       B operand; the k-range of a tile is clipped to
+//                       [j0, i_max]. Entries above the diagonal of C are not
+//                       written (the products never read them).
 //  walk_softmax_kernel  causal row softmax of t*A (the transition matrix of
 //                       the appendix lemma on the walk's stationary structure).
-//  walk_norm_kernel     divides each row by its largest magnitude.
+//  walk_norm_kernel     divides each row by its largest magnitude and writes
+//                       the zeros above the diagonal.
 //
 // Weight transforms (template parameter): the element-wise power (A/c)^s of
 // Alg. 1 step 6, the same power after clipping negative scores to zero, or
@@ -110,28 +112,52 @@ __global__ __launch_bounds__(256) void walk_gemm_kernel(const double* __restrict
   while (s + 1 < m.n_seqs && m.aux_start[s + 1] <= tile) ++s;
   const int b = m.blk_start[s + 1] - m.blk_start[s];
   const int tb = (b + 15) >> 4;
+  // Lower tiles only, longest k-range first: group g = 0, 1, ... holds the
+  // g + 1 tiles of diagonal ti - tj = tb - 1 - g.
   const int lt = tile - m.aux_start[s];
-  const int ti = lt / tb, tj = lt % tb;
+  int g = (int)((sqrt(8.0 * lt + 1.0) - 1.0) * 0.5);
+  while ((g + 1) * (g + 2) / 2 <= lt) ++g;
+  while (g * (g + 1) / 2 > lt) --g;
+  const int tj = lt - g * (g + 1) / 2;
+  const int ti = tj + tb - 1 - g;
   const double* As = A + m.mat_start[s];
   const double* Ps = Rp + m.mat_start[s];
   double* Rs = R + m.mat_start[s];
-  if (tj > ti) {
-    for (int v = 0; v < 4; ++v) {
-      const int ri = ti * 16 + (l >> 4) + 4 * v, cj = tj * 16 + (l & 15);
-      if (ri < b && cj < b) Rs[(long long)ri * b + cj] = 0.0;
-    }
-    return;
-  }
   const double inv_c = F == kWIdent ? 1.0 : 1.0 / scale_of(A_scale, s);
   const int ra = ti * 16 + (l & 15);   // A-operand row (output row)
   const int cb = tj * 16 + (l & 15);   // B-operand column (output column)
   const int kend = min(ti * 16 + 15, b - 1);
+  // 32 k per chunk, 8 MFMA steps; in step u, lane group q = l / 16 carries
+  // k = k0 + 8 q + u (the sum runs over every k once, in any order), so each
+  // lane reads 8 consecutive entries of its A row. Chunks are double-buffered
+  // in registers: the loads of the next chunk are in flight during the MFMAs
+  // of the current one.
+  const int kq = l >> 4;
+  const long long rowA = (long long)ra * b;
+  auto load = [&](int k0, double (&av)[8], double (&bv)[8]) {
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int k = k0 + 8 * kq + u;
+      av[u] = (ra < b && k <= ra) ? Ps[rowA + k] : 0.0;
+      bv[u] = (k < b && cb <= k) ? As[(long long)k * b + cb] : 0.0;
+    }
+  };
   f64x4 acc = {0.0, 0.0, 0.0, 0.0};
-  for (int k0 = (tj * 16) & ~3; k0 <= kend; k0 += 4) {
-    const int k = k0 + (l >> 4);
-    const double av = (ra < b && k <= ra) ? Ps[(long long)ra * b + k] : 0.0;
-    const double bv = (k < b && cb <= k) ? weight_of<F>(As[(long long)k * b + cb], inv_c, s_exp) : 0.0;
-    acc = __builtin_amdgcn_mfma_f64_16x16x4f64(av, bv, acc, 0, 0, 0);
+  auto compute = [&](const double (&av)[8], const double (&bv)[8]) {
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      acc = __builtin_amdgcn_mfma_f64_16x16x4f64(av[u], weight_of<F>(bv[u], inv_c, s_exp), acc, 0,
+                                                 0, 0);
+  };
+  double a0[8], b0[8], a1[8], b1[8];
+  int k0 = tj * 16;
+  load(k0, a0, b0);
+  for (; k0 <= kend; k0 += 64) {
+    if (k0 + 32 <= kend) load(k0 + 32, a1, b1);
+    compute(a0, b0);
+    if (k0 + 32 > kend) break;
+    if (k0 + 64 <= kend) load(k0 + 64, a0, b0);
+    compute(a1, b1);
   }
   for (int v = 0; v < 4; ++v) {
     const int ri = ti * 16 + (l >> 4) + 4 * v, cj = tj * 16 + (l & 15);
@@ -176,10 +202,8 @@ __global__ __launch_bounds__(256) void walk_norm_kernel(SeqMeta m, double* __res
   double mx = 0.0;
   for (int j = threadIdx.x; j <= i; j += 256) mx = fmax(mx, fabs(Rr[j]));
   mx = block_max_256(mx, tmp);
-  if (mx > 0.0) {
-    const double inv = 1.0 / mx;
-    for (int j = threadIdx.x; j <= i; j += 256) Rr[j] = Rr[j] * inv;
-  }
+  const double inv = mx > 0.0 ? 1.0 / mx : 1.0;
+  for (int j = threadIdx.x; j < b; j += 256) Rr[j] = (j <= i) ? Rr[j] * inv : 0.0;
 }
 
 namespace {
@@ -191,13 +215,14 @@ int gemm_tiles(const SeqMeta& meta, SeqMeta* m2) {
     m2->aux_start[s] = total;
     const int b = meta.blk_start[s + 1] - meta.blk_start[s];
     const int tb = (b + 15) / 16;
-    total += tb * tb;
+    total += tb * (tb + 1) / 2;
   }
   m2->aux_start[meta.n_seqs] = total;
   return total;
 }
 
-// C = X W(Y): X, Y, C lower triangular per sequence; C covers every entry.
+// C = X W(Y): X, Y, C lower triangular per sequence; only the lower
+// triangle of C (and the diagonal tiles) is written.
 template <int F>
 void gemm(const double* X, const double* Y, const double* A_scale, int s_exp, const SeqMeta& m2,
           int total, double* C, hipStream_t st) {
