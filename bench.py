@@ -655,6 +655,172 @@ def run_walk_variants(args, dev) -> dict:
                     "uses logit scale sqrt(r/d)"}
 
 
+def block_attention_mass(Q, K, B: int, chunk: int = 2048):
+    """Dense causal attention mass between blocks of one sequence, averaged
+    over the query heads and over the query tokens of each block:
+    M[i][j] = mean over heads u and tokens t of query block i of the softmax
+    probability (scale 1/sqrt(d), keys k <= t) that falls in key block j.
+    Rows sum to 1. Q [h_q][n][d], K [h_kv][n][d]; fp32 arithmetic, fp64 sums.
+    Ground truth for the ablation's mass recall (an evaluation, not a step of
+    the method)."""
+    import torch
+    h_q, n, d = Q.shape
+    G = h_q // K.shape[0]
+    b = -(-n // B)
+    dev = Q.device
+    M = torch.zeros((b, b), dtype=torch.float64, device=dev)
+    chunk = max(B, chunk // B * B)
+    for u in range(h_q):
+        Kg = K[u // G].float()
+        for c0 in range(0, n, chunk):
+            c1 = min(n, c0 + chunk)
+            sc = (Q[u, c0:c1].float() @ Kg[:c1].T) * (1.0 / math.sqrt(d))
+            tq = torch.arange(c0, c1, device=dev).unsqueeze(1)
+            tk = torch.arange(c1, device=dev).unsqueeze(0)
+            sc.masked_fill_(tk > tq, float("-inf"))
+            pr = torch.softmax(sc, dim=1)
+            nkb = -(-c1 // B)
+            pr = torch.nn.functional.pad(pr, (0, nkb * B - c1)).view(c1 - c0, nkb, B).sum(-1)
+            qb = torch.arange(c0, c1, device=dev) // B
+            M[:, :nkb].index_add_(0, qb, pr.double())
+    cnt = torch.full((b,), float(B), dtype=torch.float64, device=dev)
+    cnt[-1] = n - (b - 1) * B
+    return M / (cnt[:, None] * h_q)
+
+
+def selection_mask(idx, cnt, b: int):
+    """[b][b] bool: row i marks the key blocks selected for query block i."""
+    import torch
+    k = idx.shape[1]
+    valid = torch.arange(k, device=idx.device)[None, :] < cnt[:, None].long()
+    mask = torch.zeros((b, b + 1), dtype=torch.bool, device=idx.device)
+    cols = torch.where(valid, idx.long(), torch.full_like(idx.long(), b))
+    mask.scatter_(1, cols, True)
+    return mask[:, :b]
+
+
+def best_mask(M, pct: int):
+    """Per query block, the forced blocks {0, i} plus the key blocks of
+    largest true mass up to the same budget tau_i = ceil((i + 1) pct / 100):
+    the most attention mass any block selection of that size can cover."""
+    import torch
+    b = M.shape[0]
+    Mh = M.cpu().numpy()
+    mask = np.zeros((b, b), dtype=bool)
+    for i in range(b):
+        forced = {0, i}
+        tau = min(max(((i + 1) * pct + 99) // 100, len(forced)), i + 1)
+        rest = sorted((j for j in range(i + 1) if j not in forced), key=lambda j: (-Mh[i, j], j))
+        for j in list(forced) + rest[:tau - len(forced)]:
+            mask[i, j] = True
+    return torch.from_numpy(mask).to(M.device)
+
+
+def run_ablation(args, dev) -> dict:
+    """Recall of the block selection on synthetic data, one factor
+    at a time around the default (r = 64, s = 8, 20 %, walk across layers,
+    element-wise power): the sketch dimension r, the exponent s, the density,
+    the cross-layer walk (off = each layer ranks its own W), and the walk
+    transition. Two measures per configuration, averaged over layers:
+    mass recall = the share of the dense attention mass (all query heads)
+    that the selected blocks hold; needle recall = the share of planted
+    needle blocks selected for the query block that holds the needle's
+    query. "best" rows select by the true mass itself (an upper bound at
+    each density)."""
+    import torch
+    import synth
+    from paper_2602_07397_amd import binding as sw
+
+    w = synth.scaled(synth.WORKLOADS["llama8b"], seqlens=(args.ablation_tokens,),
+                     layers=args.ablation_layers, needles=args.ablation_needles)
+    n, B, d = w.seqlens[0], w.B, w.d
+    b = -(-n // B)
+    cu = synth.cu_seqlens(w.seqlens)
+    base = dict(r=64, s=8, pct=20, walk=True, variant=sw.WALK_POWER)
+    names = {sw.WALK_POWER: "power", sw.WALK_RELU: "relu_power", sw.WALK_SOFTMAX: "row_softmax",
+             sw.WALK_MATPOW: "matrix_power"}
+    configs = [("default", "-", dict(base))]
+    for r in (16, 32, 128):
+        configs.append(("r", r, dict(base, r=r)))
+    for s_ in (1, 2, 4, 16):
+        configs.append(("s", s_, dict(base, s=s_)))
+    for pct in (10, 30, 50, 100):
+        configs.append(("pct", pct, dict(base, pct=pct)))
+    configs.append(("walk", "off", dict(base, walk=False)))
+    for v in (sw.WALK_RELU, sw.WALK_SOFTMAX, sw.WALK_MATPOW):
+        configs.append(("variant", names[v], dict(base, variant=v)))
+    rs = sorted({c["r"] for _, _, c in configs})
+    srht = {}
+    for r in rs:
+        sg, cl = synth.srht_params(d, r, w.seed)
+        srht[r] = (torch.from_numpy(sg).to(dev), torch.from_numpy(cl).to(dev))
+    state = [None] * len(configs)
+    acc = [dict(mass=0.0, needle_hits=0, needles=0, density=0.0) for _ in configs]
+    best = {p: dict(mass=0.0, needle_hits=0, needles=0) for p in sorted({c["pct"] for _, _, c in configs})}
+    causal_pairs = b * (b + 1) / 2
+    t0 = time.perf_counter()
+    for layer in range(w.layers):
+        if args.ablation_data == "topics":
+            Q, K, _ = synth.topic_layer_inputs(w, layer, device=dev, drift=args.ablation_drift)
+            plan = []
+        else:
+            Q, K, _ = synth.prefill_layer_inputs(w, layer, device=dev)
+            # a later needle in the same key block overwrites an earlier one
+            plan = sorted({jstar: p for jstar, p in synth.needle_plan(w, layer)[0]}.items())
+        M = block_attention_mass(Q, K, B)
+        best_masks = {pct: best_mask(M, pct) for pct in best}
+        sks = {r: sw.sketch_scores(Q, K, cu, B, *srht[r]) for r in rs}
+        del Q, K
+        for ci, (_, _, c) in enumerate(configs):
+            sk = sks[c["r"]]
+            R = sw.walk_update_variant(c["variant"], sk["A"], sk["A_scale"], c["s"], cu, B,
+                                       state[ci] if c["walk"] else None,
+                                       logit_scale=math.sqrt(c["r"] / d))
+            state[ci] = R
+            idx, cnt, _ = sw.select_topk_blocks(R, cu, B, density_pct=c["pct"])
+            mask = selection_mask(idx, cnt, b)
+            a = acc[ci]
+            a["mass"] += float((M * mask).sum(dim=1).mean())
+            a["density"] += float(cnt.sum()) / causal_pairs
+            a["best_overlap"] = a.get("best_overlap", 0.0) + float(
+                (mask & best_masks[c["pct"]]).sum()) / float(best_masks[c["pct"]].sum())
+            mh = mask.cpu().numpy()
+            for (jstar, p) in plan:
+                a["needles"] += 1
+                a["needle_hits"] += int(mh[p // B, jstar])
+        for pct, bacc in best.items():
+            bm = best_masks[pct]
+            bacc["mass"] += float((M * bm).sum(dim=1).mean())
+            bmh = bm.cpu().numpy()
+            for (jstar, p) in plan:
+                bacc["needles"] += 1
+                bacc["needle_hits"] += int(bmh[p // B, jstar])
+        print(f"[bench] ablation layer {layer} done ({time.perf_counter() - t0:.1f} s)",
+              file=sys.stderr, flush=True)
+    L = w.layers
+    rows = []
+    for (axis, value, c), a in zip(configs, acc):
+        rows.append({"axis": axis, "value": value, "r": c["r"], "s": c["s"], "pct": c["pct"],
+                     "walk": c["walk"], "variant": names[c["variant"]],
+                     "mass_recall": round(a["mass"] / L, 4),
+                     "best_overlap": round(a["best_overlap"] / L, 4),
+                     "needle_recall": (round(a["needle_hits"] / a["needles"], 4)
+                                       if a["needles"] else None),
+                     "selected_fraction": round(a["density"] / L, 4)})
+    for pct, bacc in best.items():
+        rows.append({"axis": "best", "value": pct, "pct": pct,
+                     "mass_recall": round(bacc["mass"] / L, 4),
+                     "needle_recall": (round(bacc["needle_hits"] / bacc["needles"], 4)
+                                       if bacc["needles"] else None)})
+    return {"rows": rows,
+            "workload": {"tokens": n, "layers": L, "h_q": w.h_q, "h_kv": w.h_kv, "d": d, "B": B,
+                         "data": args.ablation_data, "dtype": w.dtype,
+                         "topic_drift": args.ablation_drift if args.ablation_data == "topics" else None,
+                         "needles_per_layer": w.needles if args.ablation_data == "planted" else 0},
+            "note": "synthetic data; recall is measured against the dense attention of the same "
+                    "inputs; best_overlap = share of the best-by-mass selection's blocks kept"}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -670,6 +836,17 @@ def main() -> int:
     ap.add_argument("--speedup", action="store_true",
                     help="instead of the benchmark line, print sparse-vs-dense ratios at several lengths")
     ap.add_argument("--speedup-lengths", default="16384,32768,65536,131072")
+    ap.add_argument("--ablation", action="store_true",
+                    help="instead of the benchmark line, print selection recall on planted "
+                         "synthetic data against r, s, density, walk on/off and transition")
+    ap.add_argument("--ablation-tokens", type=int, default=16384)
+    ap.add_argument("--ablation-layers", type=int, default=4)
+    ap.add_argument("--ablation-needles", type=int, default=16)
+    ap.add_argument("--ablation-drift", type=float, default=0.0,
+                    help="topic data: share of blocks that change topic at each layer")
+    ap.add_argument("--ablation-data", choices=("topics", "planted"), default="topics",
+                    help="block-topic data with heavy-tailed attention, or the benchmark's "
+                         "planted sink / local window / needles")
     ap.add_argument("--walk-variants", action="store_true",
                     help="instead of the benchmark line, time the walk transition variants at the "
                          "--speedup-lengths")
@@ -694,6 +871,9 @@ def main() -> int:
         return 0
     if args.speedup:
         print(json.dumps({"speedup": run_speedup(args, dev)}), flush=True)
+        return 0
+    if args.ablation:
+        print(json.dumps({"ablation": run_ablation(args, dev)}), flush=True)
         return 0
     if args.walk_variants:
         print(json.dumps({"walk_variants": run_walk_variants(args, dev)}), flush=True)

@@ -150,6 +150,16 @@ def _layer_seed(w: Workload, layer: int, salt: int = 0) -> int:
     return (w.seed * 1009 + layer * 17 + salt) % (2**62)
 
 
+def needle_plan(w: Workload, layer: int,
+                seqlens: Optional[Sequence[int]] = None) -> List[List[Tuple[int, int]]]:
+    """The planted needles of one layer, per sequence: (key block j*, query
+    position p) pairs, positions relative to the sequence start. Draws the
+    same numbers as prefill_layer_inputs."""
+    seqlens = tuple(seqlens if seqlens is not None else w.seqlens)
+    rng = np.random.default_rng(_layer_seed(w, layer, 1))
+    return [_needle_plan(rng, n, w.B, w.needles) for n in seqlens]
+
+
 def prefill_layer_inputs(w: Workload, layer: int, device="cpu",
                          seqlens: Optional[Sequence[int]] = None,
                          keep_fp32: bool = False):
@@ -203,6 +213,37 @@ def _plant(w: Workload, Q, K, a: int, n: int, G: int, rng, gen) -> None:
             tok = torch.repeat_interleave(scale, B)[:n]
             K[g, a:a + n] *= tok[:, None]
         del qg
+
+
+def topic_layer_inputs(w: Workload, layer: int, device="cpu", topics: int = 16,
+                       logit_boost: float = 3.0, drift: float = 0.25):
+    """Q, K, V [heads][n][d] of one layer with block-coherent, heavy-tailed
+    attention (the structure the paper's analysis assumes), for accuracy
+    ablations. Every block of tokens carries a topic; a token's query and key
+    are N(0, 1) plus a * u_topic with unit topic vectors u shared by all
+    layers and heads and a^2 = logit_boost * sqrt(d), so a query and a key of
+    the same topic gain about ``logit_boost`` in q.k / sqrt(d). Block topics
+    persist across layers; at each layer a fraction ``drift`` of the blocks
+    draws a new topic. One sequence (w.seqlens[0] tokens)."""
+    n = int(w.seqlens[0])
+    b = -(-n // w.B)
+    rng0 = np.random.default_rng(w.seed + 31)
+    U = rng0.normal(size=(topics, w.d))
+    U /= np.linalg.norm(U, axis=1, keepdims=True)
+    z = rng0.integers(0, topics, size=b)
+    for ell in range(1, layer + 1):
+        rl = np.random.default_rng(_layer_seed(w, ell, 2))
+        redraw = rl.uniform(size=b) < drift
+        z = np.where(redraw, rl.integers(0, topics, size=b), z)
+    a = float(np.sqrt(logit_boost * np.sqrt(w.d)))
+    dev = torch.device(device)
+    tok = torch.from_numpy(a * U[np.repeat(z, w.B)[:n]]).to(dev, torch.float32)     # [n][d]
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(_layer_seed(w, layer, 3))
+    Q = torch.randn((w.h_q, n, w.d), generator=gen, device=dev, dtype=torch.float32) + tok
+    K = torch.randn((w.h_kv, n, w.d), generator=gen, device=dev, dtype=torch.float32) + tok
+    V = torch.randn((w.h_kv, n, w.d), generator=gen, device=dev, dtype=torch.float32)
+    return Q.to(w.torch_dtype), K.to(w.torch_dtype), V.to(w.torch_dtype)
 
 
 def decode_prefix_inputs(w: Workload, layer: int, seq: int, device="cpu",
