@@ -317,6 +317,38 @@ int sw_sparse_attn_decode(int dtype, const void* q, const void* Kc, const void* 
                           const int32_t* idx, const int32_t* cnt, int kmax, float scale, void* O,
                           void* workspace, int64_t workspace_bytes, void* stream);
 
+/*
+ * sw_decode_step - one decode step of every layer in one call: Alg. 2 steps
+ * 1-7 for layer 0, 1, ..., layers-1 in order (the walk row of layer l starts
+ * from that of layer l-1; layer 0 is the first walked layer). Per layer it
+ * enqueues the same arithmetic as sw_kv_append + sw_sketch_scores_decode +
+ * sw_walk_update_decode_variant + sw_select_topk_blocks_decode +
+ * sw_sparse_attn_decode, with the KV append fused into the incremental sketch
+ * and the walk row's normalisation fused into the selection (4 + 1 kernel
+ * launches per layer instead of 8), so results are bit-identical to those
+ * calls.
+ *
+ * Layer-stacked, contiguous buffers (device):
+ *   q_new [layers][batch][h_q][d], k_new, v_new [layers][batch][h_kv][d]
+ *   (input dtype, 16-byte aligned); Kc, Vc [layers][batch][h_kv][T_max][d]
+ *   (updated at pos); state [layers][sw_decode_state_bytes(batch, d, r,
+ *   b_max)] (updated); rows [layers][batch][b_max] float64 walk rows (out);
+ *   idx [layers][batch][kmax], cnt [layers][batch] selections (out); O
+ *   [layers][batch][h_q][d] attention outputs (out, input dtype).
+ * T_max <= b_max * B; walk_variant SW_WALK_POWER or SW_WALK_RELU; other
+ * arguments as in the per-layer calls. workspace: >=
+ * sw_decode_step_workspace_bytes(...) bytes, 256-byte aligned, reused by
+ * every layer in stream order. The call only enqueues work on `stream`; it
+ * may be captured into a HIP graph.
+ */
+int64_t sw_decode_step_workspace_bytes(int batch, int h_q, int h_kv, int d);
+int sw_decode_step(int dtype, int layers, int batch, int h_q, int h_kv, int d, int r, int T_max,
+                   int B, int b_max, const void* q_new, const void* k_new, const void* v_new,
+                   void* Kc, void* Vc, void* state, const int32_t* pos, const int8_t* signs,
+                   const int32_t* cols, int s, int walk_variant, int k, int density_pct,
+                   uint32_t flags, int kmax, float scale, double* rows, int32_t* idx, int32_t* cnt,
+                   void* O, void* workspace, int64_t workspace_bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

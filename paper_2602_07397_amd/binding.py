@@ -68,6 +68,11 @@ _SIGNATURES = {
     "sw_select_topk_blocks_decode": (_c_int, [_vp, _c_int, _c_int, _c_int, _vp, _c_int, _c_int,
                                               ctypes.c_uint32, _vp, _vp, _c_int, _vp]),
     "sw_decode_attn_workspace_bytes": (_c_i64, [_c_int, _c_int, _c_int, _c_int]),
+    "sw_decode_step_workspace_bytes": (_c_i64, [_c_int, _c_int, _c_int, _c_int]),
+    "sw_decode_step": (_c_int, [_c_int, _c_int, _c_int, _c_int, _c_int, _c_int, _c_int, _c_int,
+                                _c_int, _c_int, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
+                                _c_int, _c_int, _c_int, _c_int, ctypes.c_uint32, _c_int,
+                                ctypes.c_float, _vp, _vp, _vp, _vp, _vp, _c_i64, _vp]),
     "sw_sparse_attn_decode": (_c_int, [_c_int, _vp, _vp, _vp, _c_int, _c_int, _c_int, _c_int, _c_int,
                                        _c_int, _vp, _vp, _vp, _c_int, ctypes.c_float, _vp, _vp, _c_i64,
                                        _vp]),
@@ -427,3 +432,47 @@ def sparse_attn_decode(q: torch.Tensor, Kc: torch.Tensor, Vc: torch.Tensor, B: i
                                       workspace.numel(), _stream(dev))
     _check(rc, "sw_sparse_attn_decode")
     return O
+
+
+def decode_step(q_new: torch.Tensor, k_new: torch.Tensor, v_new: torch.Tensor, Kc: torch.Tensor,
+                Vc: torch.Tensor, state: torch.Tensor, pos: torch.Tensor, signs: torch.Tensor,
+                cols: torch.Tensor, B: int, b_max: int, s: int = 8, walk_variant: int = WALK_POWER,
+                k: int = 0, density_pct: int = 20, flags: int = FORCE_BOTH,
+                kmax: Optional[int] = None, scale: float = 0.0, out: Optional[dict] = None,
+                workspace: Optional[torch.Tensor] = None) -> dict:
+    """One decode step of every layer (layer-stacked tensors):
+    q_new [L][batch][h_q][d], k_new/v_new [L][batch][h_kv][d], Kc/Vc
+    [L][batch][h_kv][T_max][d], state [L][state_bytes] uint8. Returns dict with
+    rows [L][batch][b_max], idx [L][batch][kmax], cnt [L][batch], O
+    [L][batch][h_q][d]; pre-allocated outputs may be passed in ``out``."""
+    L, batch, h_q, d = q_new.shape
+    h_kv = k_new.shape[2]
+    T_max = Kc.shape[3]
+    r = int(cols.numel())
+    dev = q_new.device
+    if kmax is None:
+        kmax = select_max_count_decode(b_max, k=k, density_pct=density_pct, flags=flags)
+    o = dict(out or {})
+    o.setdefault("rows", torch.empty((L, batch, b_max), dtype=torch.float64, device=dev))
+    o.setdefault("idx", torch.empty((L, batch, kmax), dtype=torch.int32, device=dev))
+    o.setdefault("cnt", torch.empty((L, batch), dtype=torch.int32, device=dev))
+    o.setdefault("O", torch.empty_like(q_new))
+    wsb = int(load().sw_decode_step_workspace_bytes(batch, h_q, h_kv, d))
+    if wsb < 0:
+        _check(1, "sw_decode_step_workspace_bytes")
+    if workspace is None or workspace.numel() < wsb:
+        workspace = torch.empty((max(wsb, 256),), dtype=torch.uint8, device=dev)
+    for name, t in (("k_new", k_new), ("v_new", v_new), ("Kc", Kc), ("Vc", Vc)):
+        if t.dtype != q_new.dtype:
+            raise SketchWalkError(f"{name} must have dtype {q_new.dtype}")
+    rc = load().sw_decode_step(
+        _dtype_code(q_new), L, batch, h_q, h_kv, d, r, T_max, B, b_max, _dev(q_new, "q_new"),
+        _dev(k_new, "k_new"), _dev(v_new, "v_new"), _dev(Kc, "Kc"), _dev(Vc, "Vc"),
+        _dev(state, "state", torch.uint8), _dev(pos, "pos", torch.int32),
+        _dev(signs, "signs", torch.int8), _dev(cols, "cols", torch.int32), s, walk_variant, k,
+        density_pct, flags, kmax, float(scale), _dev(o["rows"], "rows", torch.float64),
+        _dev(o["idx"], "idx", torch.int32), _dev(o["cnt"], "cnt", torch.int32),
+        _dev(o["O"], "O", q_new.dtype), _dev(workspace, "workspace"), workspace.numel(),
+        _stream(dev))
+    _check(rc, "sw_decode_step")
+    return o

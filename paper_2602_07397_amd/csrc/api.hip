@@ -473,4 +473,91 @@ int sw_sparse_attn_decode(int dtype, const void* q, const void* Kc, const void* 
   return hip_status(e, "sw_sparse_attn_decode launch");
 }
 
+int64_t sw_decode_step_workspace_bytes(int batch, int h_q, int h_kv, int d) {
+  return sw_decode_attn_workspace_bytes(batch, h_q, h_kv, d);
+}
+
+int sw_decode_step(int dtype, int layers, int batch, int h_q, int h_kv, int d, int r, int T_max,
+                   int B, int b_max, const void* q_new, const void* k_new, const void* v_new,
+                   void* Kc, void* Vc, void* state, const int32_t* pos, const int8_t* signs,
+                   const int32_t* cols, int s, int walk_variant, int k, int density_pct,
+                   uint32_t flags, int kmax, float scale, double* rows, int32_t* idx, int32_t* cnt,
+                   void* O, void* workspace, int64_t workspace_bytes, void* stream) {
+  if (dtype != SW_F32 && dtype != SW_BF16) return fail(SW_ERR_INVALID_ARG, "dtype=%d", dtype);
+  if (layers < 1) return fail(SW_ERR_INVALID_ARG, "layers=%d < 1", layers);
+  if (walk_variant == SW_WALK_SOFTMAX || walk_variant == SW_WALK_MATPOW)
+    return fail(SW_ERR_UNSUPPORTED, "walk variant %d is not available in decode", walk_variant);
+  if (walk_variant != SW_WALK_POWER && walk_variant != SW_WALK_RELU)
+    return fail(SW_ERR_INVALID_ARG, "unknown walk variant %d", walk_variant);
+  if (s < 1 || s > 64) return fail(SW_ERR_INVALID_ARG, "s=%d outside [1, 64]", s);
+  CHECK(check_heads(h_q, h_kv));
+  CHECK(check_decode_shape(batch, d, r, b_max, B));
+  const int G = h_q / h_kv;
+  if (G != 1 && G != 2 && G != 4 && G != 8)
+    return fail(SW_ERR_UNSUPPORTED, "decode attention needs h_q/h_kv in {1,2,4,8}, got %d", G);
+  if (d != 64 && d != 128) return fail(SW_ERR_UNSUPPORTED, "decode attention head dim d=%d (64 or 128)", d);
+  if (T_max < 1 || (int64_t)b_max * B < T_max)
+    return fail(SW_ERR_INVALID_ARG, "T_max=%d must be in [1, b_max * B = %lld]", T_max,
+                (long long)b_max * B);
+  CHECK(check_budget_args(k, density_pct, flags));
+  const int need_k = max_count_decode(b_max, k, density_pct, flags);
+  if (kmax < need_k) return fail(SW_ERR_INVALID_ARG, "kmax=%d < largest budget %d", kmax, need_k);
+  CHECK(check_ptr(q_new, 16, "q_new"));
+  CHECK(check_ptr(k_new, 16, "k_new"));
+  CHECK(check_ptr(v_new, 16, "v_new"));
+  CHECK(check_ptr(Kc, 16, "Kc"));
+  CHECK(check_ptr(Vc, 16, "Vc"));
+  CHECK(check_ptr(state, 256, "state"));
+  CHECK(check_ptr(pos, 4, "pos"));
+  CHECK(check_ptr(signs, 1, "signs"));
+  CHECK(check_ptr(cols, 4, "cols"));
+  CHECK(check_ptr(rows, 8, "rows"));
+  CHECK(check_ptr(idx, 4, "idx"));
+  CHECK(check_ptr(cnt, 4, "cnt"));
+  CHECK(check_ptr(O, 16, "O"));
+  const int64_t need = sw_decode_attn_workspace_bytes(batch, h_q, h_kv, d);
+  CHECK(check_ptr(workspace, 256, "workspace"));
+  if (workspace_bytes < need)
+    return fail(SW_ERR_INVALID_ARG, "workspace_bytes=%lld < required %lld",
+                (long long)workspace_bytes, (long long)need);
+  if (!(scale > 0.0f)) scale = 1.0f / sqrtf((float)d);
+  const size_t esz = dtype == SW_BF16 ? 2 : 4;
+  const int64_t q_step = (int64_t)batch * h_q * d * esz;
+  const int64_t kv_step = (int64_t)batch * h_kv * d * esz;
+  const int64_t cache_step = (int64_t)batch * h_kv * T_max * d * esz;
+  const int64_t state_step = sw::decode_layout(batch, d, r, b_max).total;
+  const int64_t row_step = (int64_t)batch * b_max;
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  const char* qb = static_cast<const char*>(q_new);
+  const char* kb = static_cast<const char*>(k_new);
+  const char* vb = static_cast<const char*>(v_new);
+  char* Kb = static_cast<char*>(Kc);
+  char* Vb = static_cast<char*>(Vc);
+  char* Sb = static_cast<char*>(state);
+  char* Ob = static_cast<char*>(O);
+  for (int l = 0; l < layers; ++l) {
+    char* stl = Sb + l * state_step;
+    void* Kl = Kb + l * cache_step;
+    void* Vl = Vb + l * cache_step;
+    double* rl = rows + l * row_step;
+    int32_t* il = idx + (int64_t)l * batch * kmax;
+    int32_t* cl = cnt + (int64_t)l * batch;
+    hipError_t e = sw::launch_decode_sketch(dtype, qb + l * q_step, kb + l * kv_step, batch, h_q,
+                                            h_kv, d, B, pos, signs, cols, r, b_max, stl, st,
+                                            vb + l * kv_step, Kl, Vl, T_max);
+    if (e == hipSuccess)
+      e = sw::launch_decode_walk(stl, batch, d, r, b_max, B, pos, s, walk_variant == SW_WALK_RELU,
+                                 l == 0 ? nullptr : rl - row_step, rl, st, /*normalize=*/false);
+    if (e == hipSuccess)
+      e = sw::launch_select_decode(rl, batch, b_max, B, pos, k, density_pct, flags, il, cl, kmax,
+                                   st, /*normalize_rows=*/rl);
+    if (e == hipSuccess)
+      e = sw::launch_attn_decode(dtype, qb + l * q_step, Kl, Vl, batch, h_q, h_kv, d, T_max, B, pos,
+                                 il, cl, kmax, scale, Ob + l * q_step,
+                                 reinterpret_cast<float*>(workspace), st);
+    if (e != hipSuccess) return hip_status(e, "sw_decode_step launch");
+  }
+  return ok();
+}
+
 }  // extern "C"

@@ -129,7 +129,9 @@ __device__ __forceinline__ float load_f32(const T* p, long long i) {
   }
 }
 
-template <typename T>
+// APPEND: also writes k_new and v_new into the caches at pos (Alg. 2 step 1;
+// Kc, Vc [batch][h_kv][T_max][d], 16-byte aligned rows).
+template <typename T, bool APPEND>
 __global__ __launch_bounds__(256) void decode_reps_kernel(const T* __restrict__ q_new,
                                                           const T* __restrict__ k_new, int h_q,
                                                           int h_kv, int d, int B,
@@ -137,7 +139,10 @@ __global__ __launch_bounds__(256) void decode_reps_kernel(const T* __restrict__ 
                                                           const int8_t* __restrict__ signs,
                                                           const int32_t* __restrict__ cols, int r,
                                                           int batch, int b_max,
-                                                          char* __restrict__ state) {
+                                                          char* __restrict__ state,
+                                                          const T* __restrict__ v_new,
+                                                          T* __restrict__ Kc, T* __restrict__ Vc,
+                                                          int T_max) {
   constexpr int V = 16 / (int)sizeof(T);             // elements per 16-byte load
   __shared__ double xq[256], xk[256], xb[256];
   __shared__ double pq[256 * V], pk[256 * V];
@@ -146,6 +151,18 @@ __global__ __launch_bounds__(256) void decode_reps_kernel(const T* __restrict__ 
   const int t = threadIdx.x;
   const int p = pos[bi];
   const int bc = p / B;                  // open key block == query block
+  if constexpr (APPEND) {
+    if (p >= 0 && p < T_max) {
+      const int cpr = d / V;
+      for (int c = t; c < h_kv * cpr; c += 256) {
+        const int g = c / cpr, o = (c % cpr) * V;
+        const long long src = ((long long)bi * h_kv + g) * d + o;
+        const long long dst = (((long long)bi * h_kv + g) * T_max + p) * d + o;
+        *reinterpret_cast<uint4*>(Kc + dst) = *reinterpret_cast<const uint4*>(k_new + src);
+        *reinterpret_cast<uint4*>(Vc + dst) = *reinterpret_cast<const uint4*>(v_new + src);
+      }
+    }
+  }
   if (p < 0 || bc >= b_max) return;
   double* bar = reinterpret_cast<double*>(state + L.bar) + (long long)bi * 2 * d;
   int32_t* cnt = reinterpret_cast<int32_t*>(state + L.cnt) + bi * 2;
@@ -881,19 +898,37 @@ hipError_t launch_kv_append(int dtype, const void* k_new, const void* v_new, voi
   return hipGetLastError();
 }
 
+namespace {
+
+template <typename T>
+void launch_reps(const void* q_new, const void* k_new, int batch, int h_q, int h_kv, int d, int B,
+                 const int32_t* pos, const int8_t* signs, const int32_t* cols, int r, int b_max,
+                 char* state, const void* v_new, void* Kc, void* Vc, int T_max, hipStream_t st) {
+  const T* q = reinterpret_cast<const T*>(q_new);
+  const T* k = reinterpret_cast<const T*>(k_new);
+  const T* v = reinterpret_cast<const T*>(v_new);
+  if (Kc != nullptr)
+    hipLaunchKernelGGL((decode_reps_kernel<T, true>), dim3((unsigned)batch), dim3(256), 0, st, q, k,
+                       h_q, h_kv, d, B, pos, signs, cols, r, batch, b_max, state, v,
+                       reinterpret_cast<T*>(Kc), reinterpret_cast<T*>(Vc), T_max);
+  else
+    hipLaunchKernelGGL((decode_reps_kernel<T, false>), dim3((unsigned)batch), dim3(256), 0, st, q, k,
+                       h_q, h_kv, d, B, pos, signs, cols, r, batch, b_max, state, v,
+                       static_cast<T*>(nullptr), static_cast<T*>(nullptr), T_max);
+}
+
+}  // namespace
+
 hipError_t launch_decode_sketch(int dtype, const void* q_new, const void* k_new, int batch, int h_q,
                                 int h_kv, int d, int B, const int32_t* pos, const int8_t* signs,
                                 const int32_t* cols, int r, int b_max, char* state,
-                                hipStream_t st) {
+                                hipStream_t st, const void* v_new, void* Kc, void* Vc, int T_max) {
   if (dtype == SW_BF16)
-    hipLaunchKernelGGL(decode_reps_kernel<uint16_t>, dim3((unsigned)batch), dim3(256), 0, st,
-                       reinterpret_cast<const uint16_t*>(q_new),
-                       reinterpret_cast<const uint16_t*>(k_new), h_q, h_kv, d, B, pos, signs, cols,
-                       r, batch, b_max, state);
+    launch_reps<uint16_t>(q_new, k_new, batch, h_q, h_kv, d, B, pos, signs, cols, r, b_max, state,
+                          v_new, Kc, Vc, T_max, st);
   else
-    hipLaunchKernelGGL(decode_reps_kernel<float>, dim3((unsigned)batch), dim3(256), 0, st,
-                       reinterpret_cast<const float*>(q_new), reinterpret_cast<const float*>(k_new),
-                       h_q, h_kv, d, B, pos, signs, cols, r, batch, b_max, state);
+    launch_reps<float>(q_new, k_new, batch, h_q, h_kv, d, B, pos, signs, cols, r, b_max, state,
+                       v_new, Kc, Vc, T_max, st);
   const int nch = (b_max + kScoreChunk - 1) / kScoreChunk;
   hipLaunchKernelGGL(decode_scores_kernel, dim3((unsigned)batch, (unsigned)nch), dim3(256), 0, st,
                      pos, r, B, batch, d, b_max, state);
@@ -902,7 +937,7 @@ hipError_t launch_decode_sketch(int dtype, const void* q_new, const void* k_new,
 
 hipError_t launch_decode_walk(const char* state, int batch, int d, int r, int b_max, int B,
                               const int32_t* pos, int s_exp, bool relu, const double* r_prev,
-                              double* r_out, hipStream_t st) {
+                              double* r_out, hipStream_t st, bool normalize) {
   const int nstrip = (b_max + kStrip - 1) / kStrip;
   const dim3 grid((unsigned)batch, (unsigned)nstrip), blk(kStripThreads);
   if (s_exp == 8 && !relu)
@@ -917,8 +952,9 @@ hipError_t launch_decode_walk(const char* state, int batch, int d, int r, int b_
   else
     hipLaunchKernelGGL((walk_row_strip_kernel<false, true>), grid, blk, 0, st, state, batch, d, r,
                        b_max, B, pos, s_exp, r_prev, r_out);
-  hipLaunchKernelGGL(walk_row_norm_kernel, dim3((unsigned)batch), dim3(256), 0, st, b_max, B, pos,
-                     r_out);
+  if (normalize)
+    hipLaunchKernelGGL(walk_row_norm_kernel, dim3((unsigned)batch), dim3(256), 0, st, b_max, B, pos,
+                       r_out);
   return hipGetLastError();
 }
 

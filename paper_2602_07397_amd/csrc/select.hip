@@ -158,11 +158,55 @@ __global__ __launch_bounds__(256) void select_decode_kernel(const double* __rest
                  idx + (long long)bi * kmax, cnt + bi, kmax);
 }
 
+// The same with the walk row's normalisation first: the row is divided in
+// place by its largest magnitude over blocks 0..b_cur (entries past b_cur are
+// zeroed). Each thread rescales exactly the entries select_row_dev later
+// reads in that thread (j = t*E + e), so no other thread's store is read.
+__global__ __launch_bounds__(256) void select_decode_norm_kernel(double* __restrict__ rows,
+                                                                 int b_max, int B,
+                                                                 const int32_t* __restrict__ pos,
+                                                                 int k, int pct, uint32_t flags,
+                                                                 int32_t* __restrict__ idx,
+                                                                 int32_t* __restrict__ cnt,
+                                                                 int kmax) {
+  __shared__ double tmp[4];
+  const int bi = blockIdx.x;
+  const int p = pos[bi];
+  const int bc = p / B;
+  if (p < 0 || bc >= b_max) return;
+  double* row = rows + (long long)bi * b_max;
+  const int avail = bc + 1;
+  const int E = (avail + 255) / 256;
+  const int t = threadIdx.x;
+  double mx = 0.0;
+  for (int e = 0; e < E; ++e) {
+    const int j = t * E + e;
+    if (j < avail) mx = fmax(mx, fabs(row[j]));
+  }
+  for (int off = 32; off > 0; off >>= 1) mx = fmax(mx, __shfl_xor(mx, off));
+  if ((t & 63) == 0) tmp[t >> 6] = mx;
+  __syncthreads();
+  mx = fmax(fmax(tmp[0], tmp[1]), fmax(tmp[2], tmp[3]));
+  const double inv = mx > 0.0 ? 1.0 / mx : 1.0;
+  for (int e = 0; e < E; ++e) {
+    const int j = t * E + e;
+    if (j < avail) row[j] = row[j] * inv;
+  }
+  for (int j = avail + t; j < b_max; j += 256) row[j] = 0.0;
+  const int first = (flags & SW_FORCE_FIRST) ? 0 : -1;
+  const int last = (flags & SW_FORCE_LAST) ? bc : -1;
+  select_row_dev(row, avail, first, last, k, pct, idx + (long long)bi * kmax, cnt + bi, kmax);
+}
+
 hipError_t launch_select_decode(const double* rows, int batch, int b_max, int B,
                                 const int32_t* pos, int k, int pct, uint32_t flags, int32_t* idx,
-                                int32_t* cnt, int kmax, hipStream_t st) {
-  hipLaunchKernelGGL(select_decode_kernel, dim3((unsigned)batch), dim3(256), 0, st, rows, b_max, B,
-                     pos, k, pct, flags, idx, cnt, kmax);
+                                int32_t* cnt, int kmax, hipStream_t st, double* normalize_rows) {
+  if (normalize_rows != nullptr)
+    hipLaunchKernelGGL(select_decode_norm_kernel, dim3((unsigned)batch), dim3(256), 0, st,
+                       normalize_rows, b_max, B, pos, k, pct, flags, idx, cnt, kmax);
+  else
+    hipLaunchKernelGGL(select_decode_kernel, dim3((unsigned)batch), dim3(256), 0, st, rows, b_max,
+                       B, pos, k, pct, flags, idx, cnt, kmax);
   return hipGetLastError();
 }
 

@@ -74,15 +74,19 @@ hipError_t launch_kv_append(int dtype, const void* k_new, const void* v_new, voi
 hipError_t launch_decode_sketch(int dtype, const void* q_new, const void* k_new, int batch, int h_q,
                                 int h_kv, int d, int B, const int32_t* pos, const int8_t* signs,
                                 const int32_t* cols, int r, int b_max, char* state,
-                                hipStream_t st);
+                                hipStream_t st, const void* v_new = nullptr, void* Kc = nullptr,
+                                void* Vc = nullptr, int T_max = 0);
 
 hipError_t launch_decode_walk(const char* state, int batch, int d, int r, int b_max, int B,
                               const int32_t* pos, int s_exp, bool relu, const double* r_prev,
-                              double* r_out, hipStream_t st);
+                              double* r_out, hipStream_t st, bool normalize = true);
 
+// normalize: first divide each row (in place) by its largest magnitude over
+// blocks 0..b_cur and zero the rest, as the walk row's normalisation does.
 hipError_t launch_select_decode(const double* rows, int batch, int b_max, int B,
                                 const int32_t* pos, int k, int pct, uint32_t flags, int32_t* idx,
-                                int32_t* cnt, int kmax, hipStream_t st);
+                                int32_t* cnt, int kmax, hipStream_t st,
+                                double* normalize_rows = nullptr);
 
 int decode_attn_splits(int batch, int h_kv);
 

@@ -64,6 +64,7 @@ class DecodeRun:
         r_gpu = None
         r_ref = [None] * self.batch
         stats = dict(near=0, rows=0, err=0.0, werr=0.0)
+        self.last = []                     # per layer: walk row, idx, cnt, O of this step
         for l in range(w.layers):
             q, kk, v = synth.decode_step_inputs(w, k, l, batch=self.batch)
             qd, kd, vd = U.to_dev(q), U.to_dev(kk), U.to_dev(v)
@@ -78,6 +79,7 @@ class DecodeRun:
             idx, cnt, _ = sw.select_topk_blocks_decode(r_gpu, self.B, pos, density_pct=w.pct,
                                                        kmax=self.kmax)
             out = sw.sparse_attn_decode(qd, self.Kc[l], self.Vc[l], self.B, pos, idx, cnt, self.kmax)
+            self.last.append((r_gpu.clone(), idx, cnt, out))
             if not check:
                 continue
             rg = r_gpu.cpu().numpy()

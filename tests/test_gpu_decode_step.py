@@ -1,0 +1,76 @@
+"""The one-call decode step (sw_decode_step) against the per-layer calls:
+every output of every layer and step bit-identical (the per-layer path is
+itself checked against the oracle in the same run), the caches and decode
+states bit-identical afterwards, and the clipped-power walk through the same
+call."""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from paper_2602_07397_amd import binding as sw
+
+pytestmark = pytest.mark.gpu
+
+U = pytest.importorskip("_gpu_util")
+D = pytest.importorskip("test_gpu_decode")
+
+
+def _stacked_inputs(w, k, batch):
+    qs, ks, vs = [], [], []
+    for l in range(w.layers):
+        q, kk, v = synth.decode_step_inputs(w, k, l, batch=batch)
+        qs.append(q)
+        ks.append(kk)
+        vs.append(v)
+    return (U.to_dev(torch.stack(qs)), U.to_dev(torch.stack(ks)), U.to_dev(torch.stack(vs)))
+
+
+@pytest.mark.parametrize("dtype,h_q,h_kv,d,variant", [("bf16", 8, 2, 128, sw.WALK_POWER),
+                                                      ("f32", 4, 2, 64, sw.WALK_POWER),
+                                                      ("bf16", 8, 1, 64, sw.WALK_RELU)])
+def test_decode_step_is_bit_identical_to_per_layer_calls(dtype, h_q, h_kv, d, variant):
+    w = synth.Workload("dec", 45, layers=3, h_q=h_q, h_kv=h_kv, d=d, B=64, dtype=dtype, pct=20,
+                       needles=2, batch=3, kv_len=1000, steps=70)
+    run = D.DecodeRun(w, prompts=[1000, 640, 65], steps=70, variant=variant)
+    Kc = torch.stack(run.Kc).contiguous()
+    Vc = torch.stack(run.Vc).contiguous()
+    state = torch.stack(run.state).contiguous()
+    out = None
+    ws = torch.empty((sw.load().sw_decode_step_workspace_bytes(run.batch, h_q, h_kv, d),),
+                     dtype=torch.uint8, device=U.DEV)
+    for k in range(run.steps):
+        q, kk, v = _stacked_inputs(w, k, run.batch)
+        pos = U.to_dev(np.array([n + k for n in run.prompts], dtype=np.int32))
+        out = sw.decode_step(q, kk, v, Kc, Vc, state, pos, run.ts, run.tc, run.B, run.b_max, s=w.s,
+                             walk_variant=variant, density_pct=w.pct, kmax=run.kmax, out=out,
+                             workspace=ws)
+        st = run.step(k)                           # per-layer path, checked against the oracle
+        for l, (r, idx, cnt, o) in enumerate(run.last):
+            assert torch.equal(out["rows"][l], r), (k, l)
+            assert torch.equal(out["cnt"][l], cnt), (k, l)
+            assert torch.equal(out["idx"][l], idx), (k, l)
+            assert torch.equal(out["O"][l], o), (k, l)
+        assert st["werr"] <= 1e-4 and st["err"] <= (U.ATOL_BF16 if dtype == "bf16" else U.ATOL_F32)
+    torch.cuda.synchronize()
+    for l in range(w.layers):
+        assert torch.equal(Kc[l], run.Kc[l])
+        assert torch.equal(Vc[l], run.Vc[l])
+        assert torch.equal(state[l], run.state[l])
+
+
+def test_decode_step_rejects_bad_arguments():
+    w = synth.Workload("dec", 46, layers=2, h_q=8, h_kv=2, d=128, B=64, dtype="bf16", pct=20,
+                       batch=2, kv_len=100, steps=4)
+    L, b, T = 2, 2, 128
+    q = torch.zeros((L, b, 8, 128), dtype=torch.bfloat16, device=U.DEV)
+    kv = torch.zeros((L, b, 2, 128), dtype=torch.bfloat16, device=U.DEV)
+    cache = torch.zeros((L, b, 2, T, 128), dtype=torch.bfloat16, device=U.DEV)
+    state = torch.zeros((L, sw.decode_state_bytes(b, 128, 64, 2)), dtype=torch.uint8, device=U.DEV)
+    pos = U.to_dev(np.array([100, 101], dtype=np.int32))
+    signs, cols, ts, tc = U.srht_dev(128, 64, w.seed)
+    with pytest.raises(sw.SketchWalkError, match="code 2"):
+        sw.decode_step(q, kv, kv, cache, cache.clone(), state, pos, ts, tc, 64, 2,
+                       walk_variant=sw.WALK_SOFTMAX)
+    with pytest.raises(sw.SketchWalkError, match="T_max"):
+        sw.decode_step(q, kv, kv, cache, cache.clone(), state, pos, ts, tc, 64, 1)
