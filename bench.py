@@ -41,8 +41,8 @@ FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
 MEASURED_TRAFFIC = {
     "attn_prefill.hip": ("5b49ac6e694ecec9bedc4ed002e1eb398cd5ae98dcef25c275efcc8f653ea851",
                          334395.8 * 1024, 262144.0 * 1024),
-    "decode.hip": ("2d82dfaa0e5b8ba66507ccf21dc81a4486d589f6a3bb8efbed0912d3030a4ee5",
-                   418574.4 * 1024, 1088.0 * 1024),
+    "attn_decode.hip": ("9e1117c3bdf1bef359fd82eac87052bb9945afdeb7ffa41a9b4ed20f0ebe572e",
+                        418563.7 * 1024, 1088.0 * 1024),
 }
 
 
@@ -152,9 +152,13 @@ def run_decode(args, dev) -> dict:
     ts = torch.from_numpy(signs).to(dev)
     tc = torch.from_numpy(cols).to(dev)
     t0 = time.perf_counter()
-    Kc = [torch.empty((batch, w.h_kv, T_max, w.d), dtype=torch.bfloat16, device=dev) for _ in range(L)]
-    Vc = [torch.empty_like(Kc[0]) for _ in range(L)]
-    state = [sw.new_decode_state(batch, w.d, w.r, b_max, dev) for _ in range(L)]
+    # layer-stacked caches and states (per-layer views for the setup and the
+    # per-layer launch mode)
+    Kst = torch.empty((L, batch, w.h_kv, T_max, w.d), dtype=torch.bfloat16, device=dev)
+    Vst = torch.empty_like(Kst)
+    Sst = torch.zeros((L, sw.decode_state_bytes(batch, w.d, w.r, b_max)), dtype=torch.uint8,
+                      device=dev)
+    Kc, Vc, state = list(Kst), list(Vst), list(Sst)
     for l in range(L):
         for b in range(batch):
             Q, K, V = synth.decode_prefix_inputs(w, l, b, device=dev)
@@ -184,7 +188,23 @@ def run_decode(args, dev) -> dict:
     del toks
     bq, bk, bv = torch.empty_like(tq[0]), torch.empty_like(tk[0]), torch.empty_like(tv[0])
 
+    step_out = {"rows": torch.empty((L, batch, b_max), dtype=torch.float64, device=dev),
+                "idx": torch.empty((L, batch, kmax), dtype=torch.int32, device=dev),
+                "cnt": torch.empty((L, batch), dtype=torch.int32, device=dev),
+                "O": torch.empty((L, batch, w.h_q, w.d), dtype=torch.bfloat16, device=dev)}
+    wss = torch.empty((sw.load().sw_decode_step_workspace_bytes(batch, w.h_q, w.h_kv, w.d),),
+                      dtype=torch.uint8, device=dev)
+
     def body(sel_log=None):
+        nonlocal step_out
+        if not args.decode_per_layer:
+            step_out = sw.decode_step(bq, bk, bv, Kst, Vst, Sst, pos, ts, tc, B, b_max, s=w.s,
+                                      density_pct=w.pct, kmax=kmax, out=step_out, workspace=wss)
+            if sel_log is not None:
+                for l in range(L):
+                    sel_log.append((step_out["idx"][l].clone(), step_out["cnt"][l].clone()))
+            pos.add_(1)
+            return
         r = None
         for l in range(L):
             sw.kv_append(bk[l], bv[l], Kc[l], Vc[l], pos)
@@ -267,14 +287,15 @@ def run_decode(args, dev) -> dict:
         "tok_per_s": round(wall_tok_s, 1),
         "ms_per_step": round(step_ms, 3),
         "timed_steps": n_timed, "layers": L,
-        "launch": "eager" if graph is None else "hip graph of the 32-layer step",
+        "launch": ("eager" if graph is None else "hip graph of the 32-layer step") + (
+            ", per-layer calls" if args.decode_per_layer else ", one sw_decode_step call"),
         "attention_ms_per_layer": round(attn_ms, 4),
         "rest_ms_per_layer": round(sel_ms, 4),
         "overhead_pct": round(100.0 * max(sel_ms, 0.0) / (step_ms / L), 2),
         "roofline": {
             "kernel": "attn_decode_mfma_kernel<128> + attn_merge_kernel",
             "bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-            "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": measured_traffic("decode.hip"),
+            "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": measured_traffic("attn_decode.hip"),
             "avg_launch_ms": round(attn_ms, 4), "bytes_per_launch": attn_bytes,
         },
     }
@@ -827,12 +848,14 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--layers", type=int, default=None, help="override layer count (debug only)")
-    ap.add_argument("--cpu-pairs", type=int, default=192)
+    ap.add_argument("--cpu-pairs", type=int, default=3000)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--decode-steps", type=int, default=256)
     ap.add_argument("--decode-layers", type=int, default=None, help="override (debug only)")
     ap.add_argument("--decode-eager", action="store_true", help="launch the decode step eagerly")
+    ap.add_argument("--decode-per-layer", action="store_true",
+                    help="run the decode step as per-layer calls instead of one sw_decode_step")
     ap.add_argument("--speedup", action="store_true",
                     help="instead of the benchmark line, print sparse-vs-dense ratios at several lengths")
     ap.add_argument("--speedup-lengths", default="16384,32768,65536,131072")
