@@ -225,7 +225,8 @@ int sw_sparse_attn_prefill(int dtype, const void* Q, const void* K, const void* 
  * pos [batch] int32 (device): 0-based position of the new token of each
  * sequence; b_cur = pos / B is the open block. Sequences whose pos is
  * negative, >= T_max (attention, append) or beyond b_max blocks are skipped:
- * their outputs are left untouched.
+ * their state, cache entries, walk rows and selections are left untouched,
+ * and sw_sparse_attn_decode writes zeros as their attention output.
  * ====================================================================== */
 
 /* Host-only: bytes of one layer's decode state (-1 on invalid arguments). */

@@ -74,3 +74,39 @@ def test_decode_step_rejects_bad_arguments():
                        walk_variant=sw.WALK_SOFTMAX)
     with pytest.raises(sw.SketchWalkError, match="T_max"):
         sw.decode_step(q, kv, kv, cache, cache.clone(), state, pos, ts, tc, 64, 1)
+
+
+def test_inactive_sequence_is_skipped():
+    """A sequence whose position is -1 in a step: its state, caches, walk rows
+    and selection keep their previous bytes and its attention output is zero;
+    the active sequences get exactly the bits of a step without it."""
+    w = synth.Workload("dec", 49, layers=2, h_q=8, h_kv=2, d=128, B=64, dtype="bf16", pct=20,
+                       needles=2, batch=3, kv_len=500, steps=4)
+    runs = [D.DecodeRun(w, prompts=[500, 300, 129], steps=4) for _ in range(2)]
+    outs = []
+    for which, run in enumerate(runs):
+        Kc = torch.stack(run.Kc).contiguous()
+        Vc = torch.stack(run.Vc).contiguous()
+        state = torch.stack(run.state).contiguous()
+        q, kk, v = _stacked_inputs(w, 0, run.batch)
+        pos_h = np.array([500, 300, 129], dtype=np.int32)
+        if which == 1:
+            pos_h[1] = -1
+        pos = U.to_dev(pos_h)
+        out = {"rows": torch.full((w.layers, 3, run.b_max), 7.0, dtype=torch.float64, device=U.DEV),
+               "idx": torch.full((w.layers, 3, run.kmax), 5, dtype=torch.int32, device=U.DEV),
+               "cnt": torch.full((w.layers, 3), 5, dtype=torch.int32, device=U.DEV),
+               "O": torch.full_like(q, 3.0)}
+        state0, K0 = state.clone(), Kc.clone()
+        sw.decode_step(q, kk, v, Kc, Vc, state, pos, run.ts, run.tc, run.B, run.b_max, s=w.s,
+                       density_pct=w.pct, kmax=run.kmax, out=out)
+        torch.cuda.synchronize()
+        outs.append((out, state, Kc, state0, K0))
+    full, part = outs[0], outs[1]
+    for name in ("rows", "idx", "cnt", "O"):
+        for b in (0, 2):
+            assert torch.equal(full[0][name][:, b], part[0][name][:, b]), name
+    assert torch.all(part[0]["rows"][:, 1] == 7.0)
+    assert torch.all(part[0]["idx"][:, 1] == 5) and torch.all(part[0]["cnt"][:, 1] == 5)
+    assert torch.all(part[0]["O"][:, 1] == 0)
+    assert torch.equal(part[2][:, 1], part[4][:, 1])      # cache of the skipped sequence
