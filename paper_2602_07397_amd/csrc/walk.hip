@@ -1,12 +1,14 @@
 // Sketch-Determined Walk kernels (paper Sec. 2.3, Alg. 1 step 6).
 //
 //  walk_first_kernel    first walked layer: R = W(A), row-normalised.
-//  walk_gemm_kernel     C = X W(Y) for lower triangular X, Y. One wavefront per
-//                       16x16 output tile on or below the diagonal, on fp64
-//                       MFMA 16x16x4; the weight transform W is applied to the
-//                       B operand; the k-range of a tile is clipped to
-//                       [j0, i_max]. Entries above the diagonal of C are not
-//                       written (the products never read them).
+//  walk_gemm_kernel     C = X W(Y) for lower triangular X, Y. One workgroup per
+//                       16x16 output tile on or below the diagonal, its four
+//                       wavefronts splitting the tile's k-range (clipped to
+//                       [j0, i_max]) on fp64 MFMA 16x16x4 and adding their
+//                       partial tiles in a fixed order; the weight transform W
+//                       is applied to the B operand. Entries above the
+//                       diagonal of C are not written (the products never
+//                       read them).
 //  walk_softmax_kernel  causal row softmax of t*A (the transition matrix of
 //                       the appendix lemma on the walk's stationary structure).
 //  walk_norm_kernel     divides each row by its largest magnitude and writes
@@ -104,9 +106,10 @@ __global__ __launch_bounds__(256) void walk_gemm_kernel(const double* __restrict
                                                         int s_exp, SeqMeta m, int total_tiles,
                                                         const double* __restrict__ Rp,
                                                         double* __restrict__ R) {
+  __shared__ double red[4][64][4];
   const int wave = threadIdx.x >> 6;
   const int l = threadIdx.x & 63;
-  const int tile = blockIdx.x * 4 + wave;
+  const int tile = blockIdx.x;
   if (tile >= total_tiles) return;
   int s = 0;
   while (s + 1 < m.n_seqs && m.aux_start[s + 1] <= tile) ++s;
@@ -129,9 +132,9 @@ __global__ __launch_bounds__(256) void walk_gemm_kernel(const double* __restrict
   const int kend = min(ti * 16 + 15, b - 1);
   // 32 k per chunk, 8 MFMA steps; in step u, lane group q = l / 16 carries
   // k = k0 + 8 q + u (the sum runs over every k once, in any order), so each
-  // lane reads 8 consecutive entries of its A row. Chunks are double-buffered
-  // in registers: the loads of the next chunk are in flight during the MFMAs
-  // of the current one.
+  // lane reads 8 consecutive entries of its A row. Wavefront w takes chunks
+  // w, w + 4, w + 8, ...; its chunks are double-buffered in registers: the
+  // loads of the next chunk are in flight during the MFMAs of the current one.
   const int kq = l >> 4;
   const long long rowA = (long long)ra * b;
   auto load = [&](int k0, double (&av)[8], double (&bv)[8]) {
@@ -150,18 +153,23 @@ __global__ __launch_bounds__(256) void walk_gemm_kernel(const double* __restrict
                                                  0, 0);
   };
   double a0[8], b0[8], a1[8], b1[8];
-  int k0 = tj * 16;
-  load(k0, a0, b0);
-  for (; k0 <= kend; k0 += 64) {
-    if (k0 + 32 <= kend) load(k0 + 32, a1, b1);
+  int k0 = tj * 16 + 32 * wave;
+  if (k0 <= kend) load(k0, a0, b0);
+  for (; k0 <= kend; k0 += 256) {
+    if (k0 + 128 <= kend) load(k0 + 128, a1, b1);
     compute(a0, b0);
-    if (k0 + 32 > kend) break;
-    if (k0 + 64 <= kend) load(k0 + 64, a0, b0);
+    if (k0 + 128 > kend) break;
+    if (k0 + 256 <= kend) load(k0 + 256, a0, b0);
     compute(a1, b1);
   }
+#pragma unroll
+  for (int v = 0; v < 4; ++v) red[wave][l][v] = acc[v];
+  __syncthreads();
+  if (wave != 0) return;
   for (int v = 0; v < 4; ++v) {
+    const double sum = ((red[0][l][v] + red[1][l][v]) + red[2][l][v]) + red[3][l][v];
     const int ri = ti * 16 + (l >> 4) + 4 * v, cj = tj * 16 + (l & 15);
-    if (ri < b && cj < b) Rs[(long long)ri * b + cj] = (cj <= ri) ? acc[v] : 0.0;
+    if (ri < b && cj < b) Rs[(long long)ri * b + cj] = (cj <= ri) ? sum : 0.0;
   }
 }
 
@@ -226,7 +234,7 @@ int gemm_tiles(const SeqMeta& meta, SeqMeta* m2) {
 template <int F>
 void gemm(const double* X, const double* Y, const double* A_scale, int s_exp, const SeqMeta& m2,
           int total, double* C, hipStream_t st) {
-  hipLaunchKernelGGL(walk_gemm_kernel<F>, dim3((unsigned)((total + 3) / 4)), dim3(256), 0, st, Y,
+  hipLaunchKernelGGL(walk_gemm_kernel<F>, dim3((unsigned)total), dim3(256), 0, st, Y,
                      A_scale, s_exp, m2, total, X, C);
 }
 
