@@ -325,8 +325,8 @@ int sw_sparse_attn_decode(int dtype, const void* q, const void* Kc, const void* 
  * enqueues the same arithmetic as sw_kv_append + sw_sketch_scores_decode +
  * sw_walk_update_decode_variant + sw_select_topk_blocks_decode +
  * sw_sparse_attn_decode, with the KV append fused into the incremental sketch
- * and the walk row's normalisation fused into the selection (4 + 1 kernel
- * launches per layer instead of 8), so results are bit-identical to those
+ * and the walk row's normalisation fused into the selection (6 kernel
+ * launches per layer instead of 8); results are bit-identical to those
  * calls.
  *
  * Layer-stacked, contiguous buffers (device):
