@@ -24,10 +24,10 @@ HIPFLAGS = [
     "-Wall", "-Wno-unused-result",
 ]
 
-# Per-source extras. The prefill attention kernel runs one 512-register
-# wavefront per SIMD; MFMA results it post-processes on the VALU (scores) must
-# land in VGPRs, while staging and long-lived operands go to AGPRs: the VGPR
-# form of the MFMA instructions lets the register allocator do that split.
+# Per-source extras. The prefill attention kernel post-processes its score
+# MFMA results on the VALU and runs two wavefronts per SIMD within 256
+# registers each: the VGPR form of the MFMA instructions keeps accumulators in
+# VGPRs, so no AGPR-to-VGPR copies are needed.
 EXTRA = {
     "attn_prefill.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
 }
