@@ -6,15 +6,16 @@
 //  decode_reps_kernel     steps 2-3 (one workgroup per sequence): running means
 //                         of the open query/key block, SRHT (in-LDS FWHT) of the
 //                         token query and of both open representatives
-//  decode_scores_kernel   step 4 over (sequence, 64-row chunk) workgroups, 16
-//                         lanes per 64-wide sketch row: (i) new score row (token
-//                         query vs every earlier key block), (ii) new last
-//                         column (every query block vs the open key block)
+//  decode_scores_kernel   step 4 over (sequence, 64-row chunk) workgroups, 4
+//                         lanes per sketch row: (i) new score row (token query
+//                         vs every earlier key block), (ii) new last column
+//                         (every query block vs the open key block)
 //  walk_row_strip_kernel  step 5 on the query row only: r = W[b_q, :] at the
 //                         first walked layer, else r_prev W with W = (A/c)^s
-//                         taken while streaming the fp32 score cache; one
-//                         workgroup per (sequence, 32-column strip), 32 row
-//                         groups reduced in LDS in a fixed order
+//                         (or the clipped power) taken while streaming the fp32
+//                         score cache; one workgroup per (sequence, 32-column
+//                         strip), SW_STRIP_RG row groups reduced in LDS in a
+//                         fixed order
 //  walk_row_norm_kernel   divides the row by its largest magnitude
 #include "sw_common.h"
 #include "sw_internal.h"
@@ -229,8 +230,7 @@ __global__ __launch_bounds__(256) void decode_reps_kernel(const T* __restrict__ 
 constexpr int kScoreChunk = 64;
 
 // Rows [64c, 64c+64): row entries A[bc][j] (j < bc) and column entries
-// A[m][bc] (m <= bc). 16 lanes per 64-wide row (lane sub takes elements
-// sub, sub+16, ...), 16 rows per pass of the 256 threads.
+// A[m][bc] (m <= bc), four threads per row.
 __global__ __launch_bounds__(256) void decode_scores_kernel(const int32_t* __restrict__ pos, int r,
                                                             int B, int batch, int d, int b_max,
                                                             char* __restrict__ state) {
