@@ -123,3 +123,39 @@ def test_binding_refuses_cpu_tensors():
     with pytest.raises(sw.SketchWalkError):
         sw.sparse_attn_prefill(x, x, x, [0, 64], 64, torch.zeros((1, 1), dtype=torch.int32),
                                torch.zeros(1, dtype=torch.int32), 1)
+
+
+def _compile_and_run_c(tmp_path, lang):
+    import shutil
+    import subprocess
+    cc = shutil.which("gcc" if lang == "c" else "g++")
+    if cc is None:
+        pytest.skip("no host compiler")
+    exe = str(tmp_path / f"abi_check_{lang}")
+    src = os.path.join(ROOT, "tests", "abi_check.c")
+    libdir = os.path.dirname(sw.LIB_PATH)
+    std = ["-std=c99", "-pedantic"] if lang == "c" else ["-x", "c++", "-std=c++17"]
+    cmd = [cc, *std, "-Wall", "-Wextra", "-Werror", "-I", os.path.join(ROOT, "include"), src,
+           "-L", libdir, f"-Wl,-rpath,{libdir}", "-l:libsketchwalk.so", "-o", exe]
+    subprocess.run(cmd, check=True, capture_output=True, text=True)
+    out = subprocess.run([exe], check=True, capture_output=True, text=True).stdout
+    return dict((line.split(" ", 1)[0], line.split(" ", 1)[1]) for line in out.strip().splitlines())
+
+
+@pytest.mark.parametrize("lang", ["c", "c++"])
+def test_header_compiles_and_links_from_c(tmp_path, lang):
+    """The public header compiles as C99 and as C++ with warnings as errors,
+    every call links against the built library, and the host-side answers
+    agree with the binding's."""
+    r = _compile_and_run_c(tmp_path, lang)
+    cu = [0, 100, 400]
+    assert r["version"] == "1"
+    nb, nm, mb = sw.layout(cu, 64)
+    assert r["layout"] == f"0 {nb} {nm} {mb}"
+    assert r["max_count"] == f"0 {sw.select_max_count(cu, 64, density_pct=20)}"
+    assert r["sketch_ws"] == str(sw.sketch_workspace_bytes(32, 8, 128, cu, 64))
+    assert r["walk_ws"] == f"{sw.walk_workspace_bytes(sw.WALK_MATPOW, cu, 64)} 0"
+    assert r["state_bytes"] == str(sw.decode_state_bytes(16, 128, 64, 1028))
+    assert int(r["step_ws"]) > 0
+    assert r["bad_variant"].startswith("1 ") and "variant" in r["bad_variant"]
+    assert r["too_many_blocks"] == "2"
