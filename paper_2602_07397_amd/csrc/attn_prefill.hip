@@ -35,7 +35,8 @@
 // tile ahead. The selected blocks are compacted in LDS at the start: valid
 // blocks j < i first (never masked: only a sequence's last block can be
 // partial), then the diagonal block i, whose tiles are processed without the
-// pipeline and with the causal and sequence-end masks. Work items run
+// pipeline; a wavefront skips the diagonal sub-tiles that lie after its rows
+// and masks only the one its rows cross. Work items run
 // longest-first (query blocks in descending order, the selection budget grows
 // with the block index) and the workgroups of one (query block, KV head) are
 // placed on one XCD so they share the K/V blocks through that XCD's L2.
@@ -62,31 +63,45 @@ constexpr int kPfWaves = 8;            // wavefronts per bf16 workgroup
 // work mapping
 // ---------------------------------------------------------------------------
 
-// Number of block rows with local index >= x over all sequences.
-__device__ __forceinline__ int rows_at_or_after(const SeqMeta& m, int x) {
+// Rows with local block index >= x over all sequences (x may differ per
+// lane); lane j of bl holds the block count of sequence j.
+__device__ __forceinline__ int rows_from(int bl, int n_seqs, int x) {
   int c = 0;
-  for (int s = 0; s < m.n_seqs; ++s) c += max(0, (m.blk_start[s + 1] - m.blk_start[s]) - x);
+  for (int j = 0; j < n_seqs; ++j) c += max(0, __builtin_amdgcn_readlane(bl, j) - x);
   return c;
 }
 
 // rho-th block row in longest-first order (local index descending, then
-// sequence ascending). Returns the global row and the local index.
+// sequence ascending). Returns the global row and the local index. Called by
+// whole wavefronts: the block counts are spread over the lanes (at most 64
+// sequences) and the local index is found by a 64-way search, each round
+// testing 64 candidate indices at once.
 __device__ __forceinline__ void lpt_row(const SeqMeta& m, int rho, int* row, int* s_out,
                                         int* i_out) {
+  static_assert(SW_MAX_SEQS <= 64, "one sequence per lane");
+  const int lane = threadIdx.x & 63;
+  int bl = 0;
+#pragma unroll
+  for (int j = 0; j < SW_MAX_SEQS; ++j) {
+    const int bj = m.blk_start[j + 1] - m.blk_start[j];
+    bl = (lane == j && j < m.n_seqs) ? bj : bl;
+  }
+  // invariant: the answer (largest x with rows_from(x) > rho) lies in [lo, hi]
   int lo = 0, hi = m.max_b - 1;
   while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (rows_at_or_after(m, mid) > rho) lo = mid; else hi = mid - 1;
+    const int step = (hi - lo + 63) >> 6;
+    const int x = min(hi, lo + (lane + 1) * step);
+    // rows_from decreases in x, so the passing candidates are a lane prefix
+    const int pass = __popcll(__ballot(rows_from(bl, m.n_seqs, x) > rho));
+    const int nlo = (pass == 0) ? lo : min(hi, lo + pass * step);
+    hi = (pass == 64) ? hi : min(hi, lo + (pass + 1) * step) - 1;
+    lo = nlo;
   }
   const int i = lo;
-  int k = rho - rows_at_or_after(m, i + 1);
-  int s = 0;
-  for (; s < m.n_seqs; ++s) {
-    if (m.blk_start[s + 1] - m.blk_start[s] > i) {
-      if (k == 0) break;
-      --k;
-    }
-  }
+  const int k = rho - rows_from(bl, m.n_seqs, i + 1);   // rank among sequences longer than i
+  const unsigned long long longer = __ballot(bl > i);
+  const bool mine = ((longer >> lane) & 1ull) && __popcll(longer & ((1ull << lane) - 1ull)) == k;
+  const int s = __ffsll((unsigned long long)__ballot(mine)) - 1;
   *row = m.blk_start[s] + i;
   *s_out = s;
   *i_out = i;
@@ -131,7 +146,6 @@ __global__ __launch_bounds__(kPfWaves * 64, 1) void attn_prefill_bf16_kernel(
   __shared__ __attribute__((aligned(16))) uint16_t lds[L::NST * L::STAGE];
   __shared__ int blist[SW_MAX_BLOCKS];
   __shared__ int wtot[kPfWaves];
-  __shared__ int sdiag;
 
   // ---- work item ----
   const int x = blockIdx.x;
@@ -156,9 +170,21 @@ __global__ __launch_bounds__(kPfWaves * 64, 1) void attn_prefill_bf16_kernel(
   const int u = g * G + task / WPB;        // query head (meaningful only when active)
   const int seq0 = m.tok_start[s];
   const int seq1 = m.tok_start[s + 1];
-  const int q0 = seq0 + i * BLK + (task % WPB) * 32;   // first query row of this wavefront
+  // 32-row group of the block owned by this wavefront. Wavefronts w and
+  // w + 4 share a SIMD; the upper half takes the groups in reverse order so
+  // the two hold complementary groups (g and WPB-1-g) and every SIMD has the
+  // same number of unmasked diagonal sub-tiles.
+  const int rgrp = (w >= kPfWaves / 2) ? WPB - 1 - task % WPB : task % WPB;
+  const int q0 = seq0 + i * BLK + rgrp * 32;   // first query row of this wavefront
   const bool active = (task < G * WPB) && (q0 < seq1);
   const int qpos = q0 + ln;                // this lane's query row
+
+  // The selection count and the first chunk of the selection list are
+  // loaded first, then Q: the list is needed first. The chunk lies within the
+  // row's kmax entries whatever cnt holds.
+  const int32_t* sel = idx + (long long)row * kmax;
+  const int nsel = min(cnt[row], kmax);
+  int jnext = (tid < kmax) ? sel[tid] : -1;
 
   // ---- Q fragments: lane holds query qpos, dims kk*16 + hl*8 .. +7 ----
   bf16x8 qf[D / 16];
@@ -173,31 +199,31 @@ __global__ __launch_bounds__(kPfWaves * 64, 1) void attn_prefill_bf16_kernel(
   }
 
   // ---- selected blocks, compacted: valid j < i in list order, then i ----
-  const int nsel = min(cnt[row], kmax);
-  const int32_t* sel = idx + (long long)row * kmax;
-  if (tid == 0) sdiag = 0;
-  __syncthreads();
-  int n_off = 0;
+  // Per chunk of NT entries each wavefront publishes its count of blocks
+  // j < i (low 16 bits) and whether it saw the diagonal block (bit 16).
+  int n_off = 0, sdiag = 0;
   for (int base = 0; base < nsel; base += NT) {
     const int e = base + tid;
-    const int j = (e < nsel) ? sel[e] : -1;
+    const int j = (e < nsel) ? jnext : -1;
+    jnext = (e + NT < nsel) ? sel[e + NT] : -1;
     const bool off = (j >= 0 && j < i);
-    if (j == i) sdiag = 1;
     const unsigned long long bal = __ballot(off);
+    const bool dg = __ballot(j == i) != 0ull;
     const int pre = __popcll(bal & ((1ull << l) - 1ull));
-    if (l == 0) wtot[w] = __popcll(bal);
+    if (l == 0) wtot[w] = __popcll(bal) | (dg ? 0x10000 : 0);
     __syncthreads();
     int woff = 0, tot = 0;
 #pragma unroll
     for (int q = 0; q < kPfWaves; ++q) {
-      woff += (q < w) ? wtot[q] : 0;
-      tot += wtot[q];
+      const int c = wtot[q];
+      woff += (q < w) ? (c & 0xffff) : 0;
+      tot += c & 0xffff;
+      sdiag |= c >> 16;
     }
     if (off && n_off + woff + pre < SW_MAX_BLOCKS) blist[n_off + woff + pre] = j;
     n_off = min(n_off + tot, SW_MAX_BLOCKS);
     __syncthreads();
   }
-  __syncthreads();
   const int n_blk = n_off + sdiag;
   const int ntiles = n_blk * TPB;
   const int nofft = n_off * TPB;           // tiles before the diagonal block
@@ -227,7 +253,7 @@ __global__ __launch_bounds__(kPfWaves * 64, 1) void attn_prefill_bf16_kernel(
   // Raw buffer loads through a descriptor based at the tile's first key k0
   // and sized to the end of the sequence: keys past the end read as zero
   // without per-lane tests (the diagonal-tile mask removes them).
-  auto load_tile_at = [&](int k0) SW_INL {
+  auto load_into = [&](int k0, uint4 (&kr)[KP], uint4 (&vr)[KP]) SW_INL {
     const int bytes = max(0, (seq1 - k0) * D * 2);
     const __amdgpu_buffer_rsrc_t rk =
         __builtin_amdgcn_make_buffer_rsrc((void*)(Kg + (long long)k0 * D), (short)0, bytes, kBufWord3);
@@ -236,21 +262,23 @@ __global__ __launch_bounds__(kPfWaves * 64, 1) void attn_prefill_bf16_kernel(
 #pragma unroll
     for (int p = 0; p < KP; ++p) {
       auto a = __builtin_amdgcn_raw_buffer_load_b128(rk, goff[p], 0, 0);
-      kreg[p] = __builtin_bit_cast(uint4, a);
+      kr[p] = __builtin_bit_cast(uint4, a);
       auto b = __builtin_amdgcn_raw_buffer_load_b128(rv, goff[p], 0, 0);
-      vreg[p] = __builtin_bit_cast(uint4, b);
+      vr[p] = __builtin_bit_cast(uint4, b);
     }
   };
+  auto load_tile_at = [&](int k0) SW_INL { load_into(k0, kreg, vreg); };
   auto load_tile = [&](int t) SW_INL { load_tile_at(tile_k0(t)); };
-  auto store_tile = [&](int st) SW_INL {
+  auto store_from = [&](int st, const uint4 (&kr)[KP], const uint4 (&vr)[KP]) SW_INL {
     uint16_t* ks = lds + st * L::STAGE;
     uint16_t* vs = ks + L::K_ELEMS;
 #pragma unroll
     for (int p = 0; p < KP; ++p) {
-      *reinterpret_cast<uint4*>(ks + kloff[p]) = kreg[p];
-      *reinterpret_cast<uint4*>(vs + vloff[p]) = vreg[p];
+      *reinterpret_cast<uint4*>(ks + kloff[p]) = kr[p];
+      *reinterpret_cast<uint4*>(vs + vloff[p]) = vr[p];
     }
   };
+  auto store_tile = [&](int st) SW_INL { store_from(st, kreg, vreg); };
 
   // ---- running state ----
   f32x16 oacc[D / 32];
@@ -450,36 +478,43 @@ __global__ __launch_bounds__(kPfWaves * 64, 1) void attn_prefill_bf16_kernel(
     sub_last(sY, wY, tY, vs, 2);
     next_stage();
   };
-  // diagonal-block tile, not pipelined: scores, mask, max, P, P.V per half
+  // diagonal-block tile, not pipelined: scores, mask, max, P, P.V per half.
+  // Sub-tile sub (32 keys) of the diagonal block is entirely after the rows
+  // of group rgrp when sub > rgrp (skipped: all its weights are zero) and
+  // entirely before them when sub < rgrp (no mask: those keys also precede
+  // the sequence end); only sub == rgrp is masked.
   auto tile_diag = [&](int t) SW_INL {
     stage_io(t);
     const uint16_t* kt = lds + stv * L::STAGE;
     const uint16_t* vs = kt + L::K_ELEMS;
 #pragma unroll
     for (int h2 = 0; h2 < 2; ++h2) {
-      qk_sub(kt, h2, sX);
-      mask_sub(t, h2, sX);
-      const float mx = row_max(sX);
-      if (__any(mx > mref + kRescaleSlack)) rescale_to(mx > mref + kRescaleSlack ? mx : mref);
-      uint32_t w0[4], w1[4];
-      float ts = 0.0f;
+      const int sub = (t % TPB) * 2 + h2;
+      if (active && sub <= rgrp) {
+        qk_sub(kt, h2, sX);
+        if (sub == rgrp) mask_sub(t, h2, sX);
+        const float mx = row_max(sX);
+        if (__any(mx > mref + kRescaleSlack)) rescale_to(mx > mref + kRescaleSlack ? mx : mref);
+        uint32_t w0[4], w1[4];
+        float ts = 0.0f;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) pair(sX, e, w0[e], ts);
+        for (int e = 0; e < 4; ++e) pair(sX, e, w0[e], ts);
 #pragma unroll
-      for (int e = 0; e < 4; ++e) pair(sX, 4 + e, w1[e], ts);
-      lsum += ts;
-      pv_sub(vs, w0, w1, 2 * h2);
+        for (int e = 0; e < 4; ++e) pair(sX, 4 + e, w1[e], ts);
+        lsum += ts;
+        pv_sub(vs, w0, w1, 2 * h2);
+      }
     }
     next_stage();
   };
 
   if (ntiles > 0) {
+    // tiles 0 and 1 are loaded together (a second register set), then tile 2
+    uint4 k1reg[KP], v1reg[KP];
     load_tile(0);
+    if (ntiles > 1) load_into(tile_k0(1), k1reg, v1reg);
     store_tile(0);
-    if (ntiles > 1) {
-      load_tile(1);
-      store_tile(1);
-    }
+    if (ntiles > 1) store_from(1, k1reg, v1reg);
     if (ntiles > 2) load_tile(2);
     if (ntiles > 3) k0_ahead = tile_k0(3);
     __syncthreads();
@@ -499,22 +534,38 @@ __global__ __launch_bounds__(kPfWaves * 64, 1) void attn_prefill_bf16_kernel(
   }
 
   // ---- epilogue ----
+  // The wavefront's 32 x D output rows are normalised into LDS (the K/V
+  // stages are free once every wavefront has passed the barrier) and written
+  // back row-contiguous: rows q0..q0+31 of head u are one contiguous run of
+  // O, so each 16-byte-per-lane store covers 64 / (D / 8) whole rows.
   const float ltot = sum_other_half(lsum);
-  if (!active || qpos >= seq1) return;
   const float inv = ltot > 0.0f ? 1.0f / ltot : 0.0f;
-  uint16_t* orow = O + ((long long)u * N + qpos) * D;
+  constexpr int OS = D + 8;                // output row stride in LDS (elements)
+  static_assert(kPfWaves * 32 * OS <= L::NST * L::STAGE, "output staging must fit the K/V stages");
+  __syncthreads();
+  uint16_t* ob = lds + w * 32 * OS;
 #pragma unroll
   for (int td = 0; td < D / 32; ++td) {
 #pragma unroll
     for (int jb = 0; jb < 4; ++jb) {
-      const int dv = td * 32 + jb * 8 + hl * 4;
       uint2 st;
       st.x = pack_bf16x2(oacc[td][jb * 4 + 0] * inv, oacc[td][jb * 4 + 1] * inv);
       st.y = pack_bf16x2(oacc[td][jb * 4 + 2] * inv, oacc[td][jb * 4 + 3] * inv);
-      *reinterpret_cast<uint2*>(orow + dv) = st;
+      *reinterpret_cast<uint2*>(ob + ln * OS + td * 32 + jb * 8 + hl * 4) = st;
     }
   }
-  if (lse && hl == 0)
+  if (!active) return;
+  constexpr int CPR = D / 8;               // 16-byte chunks per row
+  constexpr int RPI = 64 / CPR;            // rows per store instruction
+  const int rr = l / CPR, cc = l % CPR;
+  uint16_t* obase = O + ((long long)u * N + q0) * D;
+#pragma unroll
+  for (int it = 0; it < 32 / RPI; ++it) {
+    const int r = it * RPI + rr;
+    const uint4 v = *reinterpret_cast<const uint4*>(ob + r * OS + cc * 8);
+    if (q0 + r < seq1) *reinterpret_cast<uint4*>(obase + (long long)r * D + cc * 8) = v;
+  }
+  if (lse && hl == 0 && qpos < seq1)
     lse[(long long)u * N + qpos] = (ltot > 0.0f) ? (mref + log2f(ltot)) / kLog2e : -INFINITY;
 }
 
