@@ -34,12 +34,13 @@
 // K/V tiles of 64 keys go through three LDS stages from registers loaded one
 // tile ahead. The selected blocks are compacted in LDS at the start: valid
 // blocks j < i first (never masked: only a sequence's last block can be
-// partial), then the diagonal block i, whose tiles are processed without the
-// pipeline; a wavefront skips the diagonal sub-tiles that lie after its rows
-// and masks only the one its rows cross. Work items run
-// longest-first (query blocks in descending order, the selection budget grows
-// with the block index) and the workgroups of one (query block, KV head) are
-// placed on one XCD so they share the K/V blocks through that XCD's L2.
+// partial), then the diagonal block i. The pipeline runs on into the
+// diagonal block up to the sub-tile a wavefront's rows cross, which alone is
+// masked (causal and sequence end); the sub-tiles after it are skipped. Work
+// items run longest-first (query blocks in descending order, the selection
+// budget grows with the block index) and the workgroups of one (query block,
+// KV head) are placed on one XCD so they share the K/V blocks through that
+// XCD's L2.
 #include <type_traits>
 
 #include "sw_common.h"
@@ -54,7 +55,6 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 constexpr int KT = 64;                 // keys per LDS tile
 constexpr float kLog2e = 1.4426950408889634f;
-constexpr float kRescaleSlack = 8.0f;  // log2 units (diagonal tiles)
 constexpr float kNoRef = -1.0e30f;     // exponent reference before any key
 constexpr float kSumLimit = 65536.0f;  // bound on a pipelined P sub-tile's partial row sum
 constexpr int kPfWaves = 8;            // wavefronts per bf16 workgroup
@@ -352,15 +352,6 @@ __global__ __launch_bounds__(kPfWaves * 64, 1) void attn_prefill_bf16_kernel(
         (__attribute__((address_space(3))) i16x4*)(pp + 8 * L::VS));
     return __builtin_bit_cast(bf16x8, __builtin_shufflevector(r0, r1, 0, 1, 2, 3, 4, 5, 6, 7));
   };
-  // O^T += V^T P^T for the 16-key chunks c0, c0+1 of a tile (not pipelined)
-  auto pv_sub = [&](const uint16_t* vs, const uint32_t (&w0)[4], const uint32_t (&w1)[4], int c0) SW_INL {
-    const uint16_t* vr = vs + vlane + c0 * 16 * L::VS;
-    const bf16x8 pb[2] = {__builtin_bit_cast(bf16x8, w0), __builtin_bit_cast(bf16x8, w1)};
-#pragma unroll
-    for (int n = 0; n < NPV; ++n)
-      oacc[n % (D / 32)] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vread(vr, n), pb[n / (D / 32)],
-                                                                   oacc[n % (D / 32)], 0, 0, 0);
-  };
   // rare path: exact row max of S, new reference, rescale, recompute P(u)
   auto refix = [&](const f32x16& S, uint32_t (&w0)[4], uint32_t (&w1)[4], float& ts) SW_INL {
     rescale_to(fmaxf(mref, row_max(S)));
@@ -397,8 +388,11 @@ __global__ __launch_bounds__(kPfWaves * 64, 1) void attn_prefill_bf16_kernel(
   // One pipeline sub-step (see the header): cur = S(u) with chunk-0 words wc
   // and their partial sum tc; produces nxt = S(u+1), its chunk-0 words wn and
   // partial sum tn.
+  // tmask >= 0: S(u+1) is the wavefront's diagonal sub-tile, half h2n of
+  // tile tmask, and is masked before its exponentials.
   auto sub = [&](f32x16& cur, uint32_t (&wc)[4], float& tc, f32x16& nxt, uint32_t (&wn)[4],
-                 float& tn, const uint16_t* ksn, int h2n, const uint16_t* vs, int c0) SW_INL {
+                 float& tn, const uint16_t* ksn, int h2n, const uint16_t* vs, int c0,
+                 int tmask) SW_INL {
     const uint16_t* kr = ksn + (h2n * 32 + ln) * L::KS + hl * 8;
     const uint16_t* vr = vs + vlane + c0 * 16 * L::VS;
     uint32_t w1[4];
@@ -420,10 +414,11 @@ __global__ __launch_bounds__(kPfWaves * 64, 1) void attn_prefill_bf16_kernel(
       }
       __builtin_amdgcn_sched_barrier(0);
     }
+    if (tmask >= 0) mask_sub(tmask, h2n, nxt);
     check(cur, wc, w1, tc);
     phase_b(vr, wc, w1, vf, nxt, wn, tn, std::true_type{});
   };
-  // final sub-step of the off-diagonal run: no scores ahead
+  // final sub-step of a wavefront's run: no scores ahead
   auto sub_last = [&](f32x16& cur, uint32_t (&wc)[4], float& tc, const uint16_t* vs, int c0) SW_INL {
     const uint16_t* vr = vs + vlane + c0 * 16 * L::VS;
     uint32_t w1[4];
@@ -460,51 +455,33 @@ __global__ __launch_bounds__(kPfWaves * 64, 1) void attn_prefill_bf16_kernel(
   f32x16 sX, sY;
   uint32_t wX[4], wY[4];
   float tX = 0.0f, tY = 0.0f;
+  // Last 32-key sub-tile of this wavefront's run, counting two per tile:
+  // the off-diagonal blocks, then in the diagonal block the sub-tiles up to
+  // the one its rows cross (number rgrp; the later ones lie after all its
+  // rows and are skipped, the earlier ones precede them and need no mask).
+  // Wavefronts without rows stop after the off-diagonal blocks.
+  const int uend = 2 * nofft - 1 + ((active && sdiag) ? rgrp + 1 : 0);
   // off-diagonal tile t < nofft-1: both halves, the second computing the
-  // first half of tile t+1
+  // first half of tile t+1 (every wavefront's run goes past it)
   auto tile_step = [&](int t) SW_INL {
     stage_io(t);
     const uint16_t* kt = lds + stv * L::STAGE;
     const uint16_t* vs = kt + L::K_ELEMS;
-    sub(sX, wX, tX, sY, wY, tY, kt, 1, vs, 0);
-    sub(sY, wY, tY, sX, wX, tX, lds + stk * L::STAGE, 0, vs, 2);
+    sub(sX, wX, tX, sY, wY, tY, kt, 1, vs, 0, -1);
+    sub(sY, wY, tY, sX, wX, tX, lds + stk * L::STAGE, 0, vs, 2, -1);
     next_stage();
   };
-  auto tile_last = [&](int t) SW_INL {
+  // any later tile: each half continues, ends or skips this wavefront's run
+  auto tile_end = [&](int t) SW_INL {
     stage_io(t);
     const uint16_t* kt = lds + stv * L::STAGE;
     const uint16_t* vs = kt + L::K_ELEMS;
-    sub(sX, wX, tX, sY, wY, tY, kt, 1, vs, 0);
-    sub_last(sY, wY, tY, vs, 2);
-    next_stage();
-  };
-  // diagonal-block tile, not pipelined: scores, mask, max, P, P.V per half.
-  // Sub-tile sub (32 keys) of the diagonal block is entirely after the rows
-  // of group rgrp when sub > rgrp (skipped: all its weights are zero) and
-  // entirely before them when sub < rgrp (no mask: those keys also precede
-  // the sequence end); only sub == rgrp is masked.
-  auto tile_diag = [&](int t) SW_INL {
-    stage_io(t);
-    const uint16_t* kt = lds + stv * L::STAGE;
-    const uint16_t* vs = kt + L::K_ELEMS;
-#pragma unroll
-    for (int h2 = 0; h2 < 2; ++h2) {
-      const int sub = (t % TPB) * 2 + h2;
-      if (active && sub <= rgrp) {
-        qk_sub(kt, h2, sX);
-        if (sub == rgrp) mask_sub(t, h2, sX);
-        const float mx = row_max(sX);
-        if (__any(mx > mref + kRescaleSlack)) rescale_to(mx > mref + kRescaleSlack ? mx : mref);
-        uint32_t w0[4], w1[4];
-        float ts = 0.0f;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) pair(sX, e, w0[e], ts);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) pair(sX, 4 + e, w1[e], ts);
-        lsum += ts;
-        pv_sub(vs, w0, w1, 2 * h2);
-      }
-    }
+    const int v0 = 2 * t;
+    if (v0 + 1 <= uend) sub(sX, wX, tX, sY, wY, tY, kt, 1, vs, 0, (v0 + 1 == uend) ? t : -1);
+    else if (v0 == uend) sub_last(sX, wX, tX, vs, 0);
+    if (v0 + 2 <= uend)
+      sub(sY, wY, tY, sX, wX, tX, lds + stk * L::STAGE, 0, vs, 2, (v0 + 2 == uend) ? t + 1 : -1);
+    else if (v0 + 1 == uend) sub_last(sY, wY, tY, vs, 2);
     next_stage();
   };
 
@@ -518,19 +495,18 @@ __global__ __launch_bounds__(kPfWaves * 64, 1) void attn_prefill_bf16_kernel(
     if (ntiles > 2) load_tile(2);
     if (ntiles > 3) k0_ahead = tile_k0(3);
     __syncthreads();
-    int t = 0;
-    if (nofft > 0) {
+    if (uend >= 0) {
       // scores of the first sub-tile; its chunk-0 words are left to the
       // first check (an infinite partial sum forces the exact reference)
       qk_sub(lds, 0, sX);
+      if (uend == 0) mask_sub(0, 0, sX);
       tX = INFINITY;
 #pragma unroll
       for (int e = 0; e < 4; ++e) wX[e] = 0u;
-      for (; t + 1 < nofft; ++t) tile_step(t);
-      tile_last(t);
-      ++t;
     }
-    for (; t < ntiles; ++t) tile_diag(t);
+    int t = 0;
+    for (; t + 1 < nofft; ++t) tile_step(t);
+    for (; t < ntiles; ++t) tile_end(t);
   }
 
   // ---- epilogue ----
