@@ -1,8 +1,9 @@
 // Small-World Sketching kernels (paper Sec. 2.2, Alg. 1 steps 1-5).
 //
-//  pool_kernel    head mean + block mean: streams Q or K once from HBM with
-//                 16-byte loads; every workgroup sums one (block, head chunk)
-//                 slice in fp64 and writes a partial [d] vector.
+//  pool_kernel    head mean + block mean: streams Q and K once from HBM (one
+//                 launch) with 16-byte loads; every workgroup sums one
+//                 (block, head chunk) slice of Q or K in fp64 and writes a
+//                 partial [d] vector.
 //  fwht_kernel    per block row: fixed-order sum of the partials, divide by
 //                 heads x tokens, random signs, in-LDS fast Walsh-Hadamard
 //                 transform (natural order), column sampling, 1/sqrt(r).
@@ -16,14 +17,23 @@ namespace sw {
 
 typedef double f64x4 __attribute__((ext_vector_type(4)));
 
+// One launch pools both Q and K: workgroups [0, nb * Pq) take Q, the rest K.
 template <typename T>
-__global__ __launch_bounds__(256) void pool_kernel(const T* __restrict__ X, int hc, int P, int d,
-                                                   SeqMeta m, long long N,
-                                                   double* __restrict__ ws) {
+__global__ __launch_bounds__(256) void pool_kernel(const T* __restrict__ Xq, int hcq, int Pq,
+                                                   double* __restrict__ wsq,
+                                                   const T* __restrict__ Xk, int hck, int Pk,
+                                                   double* __restrict__ wsk, int nb, int d,
+                                                   SeqMeta m, long long N) {
   constexpr int VEC = 16 / sizeof(T);
   __shared__ double red[256 * VEC];
-  const int row = blockIdx.x / P;
-  const int p = blockIdx.x % P;
+  const bool is_q = (int)blockIdx.x < nb * Pq;
+  const int bx = is_q ? (int)blockIdx.x : (int)blockIdx.x - nb * Pq;
+  const T* X = is_q ? Xq : Xk;
+  const int hc = is_q ? hcq : hck;
+  const int P = is_q ? Pq : Pk;
+  double* ws = is_q ? wsq : wsk;
+  const int row = bx / P;
+  const int p = bx % P;
   const int s = seq_of_block(m, row);
   const int i = row - m.blk_start[s];
   const int t0 = m.tok_start[s] + i * m.B;
@@ -185,17 +195,15 @@ hipError_t launch_sketch(int dtype, const void* Q, const void* K, int h_q, int h
   double* wsq = reinterpret_cast<double*>(ws);
   const int64_t qbytes = ((nb * Pq * d * 8) + 255) / 256 * 256;
   double* wsk = reinterpret_cast<double*>(reinterpret_cast<char*>(ws) + qbytes);
-  if (dtype == SW_BF16) {
-    hipLaunchKernelGGL(pool_kernel<uint16_t>, dim3((unsigned)(nb * Pq)), dim3(256), 0, st,
-                       reinterpret_cast<const uint16_t*>(Q), hcq, Pq, d, meta, N, wsq);
-    hipLaunchKernelGGL(pool_kernel<uint16_t>, dim3((unsigned)(nb * Pk)), dim3(256), 0, st,
-                       reinterpret_cast<const uint16_t*>(K), hck, Pk, d, meta, N, wsk);
-  } else {
-    hipLaunchKernelGGL(pool_kernel<float>, dim3((unsigned)(nb * Pq)), dim3(256), 0, st,
-                       reinterpret_cast<const float*>(Q), hcq, Pq, d, meta, N, wsq);
-    hipLaunchKernelGGL(pool_kernel<float>, dim3((unsigned)(nb * Pk)), dim3(256), 0, st,
-                       reinterpret_cast<const float*>(K), hck, Pk, d, meta, N, wsk);
-  }
+  const unsigned pool_grid = (unsigned)(nb * (Pq + Pk));
+  if (dtype == SW_BF16)
+    hipLaunchKernelGGL(pool_kernel<uint16_t>, dim3(pool_grid), dim3(256), 0, st,
+                       reinterpret_cast<const uint16_t*>(Q), hcq, Pq, wsq,
+                       reinterpret_cast<const uint16_t*>(K), hck, Pk, wsk, (int)nb, d, meta, N);
+  else
+    hipLaunchKernelGGL(pool_kernel<float>, dim3(pool_grid), dim3(256), 0, st,
+                       reinterpret_cast<const float*>(Q), hcq, Pq, wsq,
+                       reinterpret_cast<const float*>(K), hck, Pk, wsk, (int)nb, d, meta, N);
   hipLaunchKernelGGL(fwht_kernel, dim3((unsigned)nb, 2), dim3(256), 0, st, wsq, wsk, Pq, Pk, h_q,
                      h_kv, d, meta, signs, cols, r, Qs, Ks, Qbar, Kbar, A_scale);
   // tile prefix per sequence
