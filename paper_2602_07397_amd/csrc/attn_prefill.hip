@@ -293,6 +293,7 @@ __global__ __launch_bounds__(kPfWaves * 64, 1) void attn_prefill_bf16_kernel(
   constexpr int NPV = 2 * (D / 32);        // P.V MFMAs per sub-tile: (chunk, dim block)
   constexpr int QK_PER_PAIR = NKK / 4;     // score MFMAs per element pair (phase A)
   constexpr int PV_PER_PAIR = NPV / 4;     // P.V MFMAs per element pair (phase B)
+  constexpr int kAhead = 3;                // K and V^T operands are read this many MFMAs ahead
   // V^T operand lane offset: lane (ln, hl) reads with ds_read_b64_tr_b16 from
   // key row c*16 + 4*hl + (ln%16)/4 (+8) and dims td*32 + 16*(ln/16) + 4*(ln%4);
   // it receives dim td*32 + ln of keys c*16 + 4*hl + 0..3 and
@@ -375,7 +376,7 @@ __global__ __launch_bounds__(kPfWaves * 64, 1) void attn_prefill_bf16_kernel(
     tn = 0.0f;
 #pragma unroll
     for (int n = 0; n < NPV; ++n) {
-      if (n + 2 < NPV) vf[n + 2] = vread(vr, n + 2);
+      if (n + kAhead < NPV) vf[n + kAhead] = vread(vr, n + kAhead);
       oacc[n % (D / 32)] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[n], pb[n / (D / 32)],
                                                                    oacc[n % (D / 32)], 0, 0, 0);
       if (HAS_NEXT && (n % PV_PER_PAIR) == PV_PER_PAIR - 1) {
@@ -398,15 +399,14 @@ __global__ __launch_bounds__(kPfWaves * 64, 1) void attn_prefill_bf16_kernel(
     uint32_t w1[4];
     bf16x8 kf[NKK];
     bf16x8 vf[NPV];
-    kf[0] = *reinterpret_cast<const bf16x8*>(kr);
-    kf[1] = *reinterpret_cast<const bf16x8*>(kr + 16);
+#pragma unroll
+    for (int q = 0; q < kAhead; ++q) kf[q] = *reinterpret_cast<const bf16x8*>(kr + q * 16);
 #pragma unroll
     for (int j = 0; j < 16; ++j) nxt[j] = 0.0f;
 #pragma unroll
     for (int kk = 0; kk < NKK; ++kk) {
-      if (kk + 2 < NKK) kf[kk + 2] = *reinterpret_cast<const bf16x8*>(kr + (kk + 2) * 16);
-      if (kk == NKK - 2) vf[0] = vread(vr, 0);
-      if (kk == NKK - 1) vf[1] = vread(vr, 1);
+      if (kk + kAhead < NKK) kf[kk + kAhead] = *reinterpret_cast<const bf16x8*>(kr + (kk + kAhead) * 16);
+      if (kk >= NKK - kAhead) vf[kk - (NKK - kAhead)] = vread(vr, kk - (NKK - kAhead));
       nxt = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[kk], qf[kk], nxt, 0, 0, 0);
       if ((kk % QK_PER_PAIR) == QK_PER_PAIR - 1) {
         const int e = kk / QK_PER_PAIR;              // 0..3
@@ -423,8 +423,8 @@ __global__ __launch_bounds__(kPfWaves * 64, 1) void attn_prefill_bf16_kernel(
     const uint16_t* vr = vs + vlane + c0 * 16 * L::VS;
     uint32_t w1[4];
     bf16x8 vf[NPV];
-    vf[0] = vread(vr, 0);
-    vf[1] = vread(vr, 1);
+#pragma unroll
+    for (int q = 0; q < kAhead; ++q) vf[q] = vread(vr, q);
 #pragma unroll
     for (int e = 0; e < 4; ++e) pair(cur, 4 + e, w1[e], tc);
     check(cur, wc, w1, tc);
