@@ -39,10 +39,10 @@ PEAK_HBM_GBS = 8000.0
 # measured on: a changed source reports null.
 FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
 MEASURED_TRAFFIC = {
-    "attn_prefill.hip": ("c2c20bfd89a5f6238f5bc2fae1f088f23b0bc339cf94dff5c29a520c36ca68bd",
-                         334102.7 * 1024, 262144.0 * 1024),
+    "attn_prefill.hip": ("ead88101fe94a31d75def7c94fd7fd367a6a5f47365fa53394bf50edc4d109e7",
+                         334161.0 * 1024, 262144.0 * 1024),
     "attn_decode.hip": ("9e1117c3bdf1bef359fd82eac87052bb9945afdeb7ffa41a9b4ed20f0ebe572e",
-                        418520.5 * 1024, 1088.0 * 1024),
+                        418559.5 * 1024, 1088.0 * 1024),
 }
 
 
