@@ -328,7 +328,9 @@ __global__ __launch_bounds__(256) void attn_decode_mfma_kernel(
       const int t0 = (step < nsteps && gi < g1) ? group_t0(gi) : -1;
       t0s[x] = t0;
       // No branch around the loads (the wait counts stay exact): a group
-      // without valid keys gets an empty descriptor and reads zeros.
+      // without valid keys gets an empty descriptor and reads zeros. The
+      // loads are non-temporal (cache policy 2): each selected K/V byte is
+      // read once per step, and the streaming hint lifts the read rate.
       const int tb = max(t0, 0);
       const int bytes = (t0 >= 0) ? (p + 1 - t0) * D * 2 : 0;   // keys past p read as zero
       const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc(
@@ -337,12 +339,12 @@ __global__ __launch_bounds__(256) void attn_decode_mfma_kernel(
           (void*)(Vb + (long long)tb * D), (short)0, bytes, kDecBufWord3);
 #pragma unroll
       for (int c = 0; c < D / 32; ++c) {
-        auto a = __builtin_amdgcn_raw_buffer_load_b128(rk, koff + c * 64, 0, 0);
+        auto a = __builtin_amdgcn_raw_buffer_load_b128(rk, koff + c * 64, 0, 2);
         kr[x][c] = __builtin_bit_cast(uint4, a);
       }
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        auto b = __builtin_amdgcn_raw_buffer_load_b128(rv, voff + r * D * 2, 0, 0);
+        auto b = __builtin_amdgcn_raw_buffer_load_b128(rv, voff + r * D * 2, 0, 2);
         vr[x][r] = __builtin_bit_cast(uint4, b);
       }
     }

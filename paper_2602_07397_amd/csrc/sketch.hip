@@ -16,6 +16,7 @@
 namespace sw {
 
 typedef double f64x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 // One launch pools both Q and K: workgroups [0, nb * Pq) take Q, the rest K.
 template <typename T>
@@ -51,7 +52,10 @@ __global__ __launch_bounds__(256) void pool_kernel(const T* __restrict__ Xq, int
     const T* base = X + ((long long)(p * hc + hh) * N) * d + lane * VEC;
 #pragma unroll 4
     for (int t = t0 + r0; t < t1; t += rpp) {
-      const uint4 v = *reinterpret_cast<const uint4*>(base + (long long)t * d);
+      // non-temporal: Q and K are streamed once here (the streaming hint
+      // lifts the read rate)
+      const u32x4 vv = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(base + (long long)t * d));
+      const uint4 v = make_uint4(vv[0], vv[1], vv[2], vv[3]);
       if constexpr (sizeof(T) == 2) {
         const uint32_t w[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
