@@ -40,9 +40,9 @@ PEAK_HBM_GBS = 8000.0
 FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
 MEASURED_TRAFFIC = {
     "attn_prefill.hip": ("ead88101fe94a31d75def7c94fd7fd367a6a5f47365fa53394bf50edc4d109e7",
-                         334161.0 * 1024, 262144.0 * 1024),
-    "attn_decode.hip": ("9e1117c3bdf1bef359fd82eac87052bb9945afdeb7ffa41a9b4ed20f0ebe572e",
-                        418559.5 * 1024, 1088.0 * 1024),
+                         334305.0 * 1024, 262144.0 * 1024),
+    "attn_decode.hip": ("35298374e364ffeab9cb07588b1482cfc8b2e768beb1ae05288389c6639aa035",
+                        419347.3 * 1024, 1088.0 * 1024),
 }
 
 
