@@ -100,7 +100,7 @@ __device__ __forceinline__ void lpt_row(const SeqMeta& m, int rho, int* row, int
   const int i = lo;
   const int k = rho - rows_from(bl, m.n_seqs, i + 1);   // rank among sequences longer than i
   const unsigned long long longer = __ballot(bl > i);
-  const bool mine = ((longer >> lane) & 1ull) && __popcll(longer & ((1ull << lane) - 1ull)) == k;
+  const bool mine = ((longer >> lane) & 1ull) && (int)__popcll(longer & ((1ull << lane) - 1ull)) == k;
   const int s = __ffsll((unsigned long long)__ballot(mine)) - 1;
   *row = m.blk_start[s] + i;
   *s_out = s;
