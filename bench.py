@@ -442,6 +442,79 @@ def run_prefill(args, dev):
     return out, cpu_layer
 
 
+def run_configs(args, dev) -> dict:
+    """The other prefill workloads, measured like the benchmark's attention
+    kernel: the single-layer stress shape at every density of its sweep and
+    the varlen batch (2 walked layers). Per layer: the whole path (sketch,
+    walk, select, attention) and the attention kernel alone, with the FLOPs
+    the selection executes."""
+    import torch
+    import synth
+    from paper_2602_07397_amd import binding as sw
+
+    out = []
+    for name in ("stress", "varlen"):
+        w = synth.WORKLOADS[name]
+        cu = synth.cu_seqlens(w.seqlens)
+        B = w.B
+        signs, cols = synth.srht_params(w.d, w.r, w.seed)
+        ts = torch.from_numpy(signs).to(dev)
+        tc = torch.from_numpy(cols).to(dev)
+        layers = [synth.prefill_layer_inputs(w, l, device=dev) for l in range(w.layers)]
+        pcts = synth.STRESS_DENSITIES if name == "stress" else (w.pct,)
+        for pct in pcts:
+            kmax = sw.select_max_count(cu, B, density_pct=pct)
+            sel = []
+
+            def path(events=None):
+                R = None
+                sel.clear()
+                for l, (Q, K, V) in enumerate(layers):
+                    sk = sw.sketch_scores(Q, K, cu, B, ts, tc)
+                    R = sw.walk_update(sk["A"], sk["A_scale"], w.s, cu, B, R)
+                    idx, cnt, _ = sw.select_topk_blocks(R, cu, B, density_pct=pct, kmax=kmax)
+                    if events is not None:
+                        events[l][0].record()
+                    sw.sparse_attn_prefill(Q, K, V, cu, B, idx, cnt, kmax)
+                    if events is not None:
+                        events[l][1].record()
+                    sel.append((idx, cnt))
+
+            path()
+            torch.cuda.synchronize(dev)
+            flops = sum(attention_flops(i.cpu().numpy(), c.cpu().numpy(), cu, B, w.h_q, w.d)[0]
+                        for i, c in sel)
+            # the same passes give both times: events around all of them and
+            # around every attention launch inside them
+            reps = 3
+            evs = [[[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in layers]
+                   for _ in range(reps)]
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for r in range(reps):
+                path(evs[r])
+            e1.record()
+            torch.cuda.synchronize(dev)
+            path_ms = e0.elapsed_time(e1) / reps
+            attn_ms = sum(a.elapsed_time(b) for er in evs for a, b in er) / reps
+            rec = {"workload": name, "layers": len(layers), "density_pct": pct,
+                   "tokens": int(cu[-1]), "sequences": len(cu) - 1,
+                   "path_ms": round(path_ms, 3), "attention_ms": round(attn_ms, 3),
+                   "executed_tflop": round(flops / 1e12, 4),
+                   "attention_tflops": round(flops / (attn_ms * 1e-3) / 1e12, 1),
+                   "attention_frac_of_peak": round(flops / (attn_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+                   "path_tflops": round(flops / (path_ms * 1e-3) / 1e12, 1),
+                   "overhead_pct": round(100.0 * (path_ms - attn_ms) / path_ms, 2)}
+            print(f"[bench] configs {rec}", file=sys.stderr, flush=True)
+            out.append(rec)
+        del layers
+        torch.cuda.empty_cache()
+    return {"prefill": out,
+            "note": "synthetic inputs of each workload's recipe; attention time from HIP events "
+                    "around the kernel, path time from events around whole passes"}
+
+
 def run_speedup(args, dev) -> dict:
     """Sparse vs dense at 16K-128K tokens (one layer of the Llama-3-8B
     shape; the paper reports only such ratios, against FlashAttention).
@@ -856,6 +929,9 @@ def main() -> int:
     ap.add_argument("--decode-eager", action="store_true", help="launch the decode step eagerly")
     ap.add_argument("--decode-per-layer", action="store_true",
                     help="run the decode step as per-layer calls instead of one sw_decode_step")
+    ap.add_argument("--configs", action="store_true",
+                    help="instead of the benchmark line, measure the stress density sweep and "
+                         "the varlen batch")
     ap.add_argument("--speedup", action="store_true",
                     help="instead of the benchmark line, print sparse-vs-dense ratios at several lengths")
     ap.add_argument("--speedup-lengths", default="16384,32768,65536,131072")
@@ -894,6 +970,9 @@ def main() -> int:
         return 0
     if args.speedup:
         print(json.dumps({"speedup": run_speedup(args, dev)}), flush=True)
+        return 0
+    if args.configs:
+        print(json.dumps({"configs": run_configs(args, dev)}), flush=True)
         return 0
     if args.ablation:
         print(json.dumps({"ablation": run_ablation(args, dev)}), flush=True)
