@@ -134,6 +134,70 @@ def cpu_baseline(Qh, Kh, Vh, cu, B, signs, cols, s, pct, pairs, seed=0):
     }
 
 
+def cpu_baseline_decode(budget_s: float = 10.0, layers: int = 4, seed: int = 0) -> dict:
+    """Times the fp64 oracle's decode (Alg. 2 steps 2-7: decode_layer_step
+    and decode_attention) for one sequence of the decode workload at its full
+    shapes, over `layers` layers and as many steps as fit in about
+    `budget_s` seconds, and scales it to tokens per second of the whole
+    batch. The per-layer state and caches hold seeded random values of the
+    workload's shapes (the oracle's work does not depend on the values); the
+    caches are built in fp64 once, outside the timed region."""
+    import oracle as O
+    import synth
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+    except Exception:  # pragma: no cover
+        cores = os.cpu_count() or 1
+    w = synth.WORKLOADS["decode"]
+    B, d, r = w.B, w.d, w.r
+    n0 = w.kv_len
+    T = n0 + w.steps
+    b_max = -(-T // B)
+    b0 = -(-n0 // B)
+    signs, cols = synth.srht_params(d, r, w.seed)
+    rng = np.random.default_rng(seed)
+    states = []
+    for _ in range(layers):
+        A = np.zeros((b_max, b_max))
+        A[:b0, :b0] = np.tril(rng.standard_normal((b0, b0)))
+        qbar = np.zeros((b_max, d))
+        kbar = np.zeros((b_max, d))
+        qbar[:b0] = rng.standard_normal((b0, d))
+        kbar[:b0] = rng.standard_normal((b0, d))
+        last = n0 - (b0 - 1) * B
+        states.append(O.DecodeLayerState(qbar, kbar, last, last, A, float(np.abs(A).max())))
+    Kc = rng.standard_normal((w.h_kv, T, d))
+    Vc = rng.standard_normal((w.h_kv, T, d))
+    t0 = time.perf_counter()
+    done = 0
+    p = n0
+    while True:
+        r_prev = None
+        for st in states:
+            q_new = rng.standard_normal((w.h_q, d))
+            k_new = rng.standard_normal((w.h_kv, d))
+            row, sel, _ = O.decode_layer_step(st, q_new, k_new, p, r_prev, B, signs, cols, w.s,
+                                              pct=w.pct)
+            O.decode_attention(q_new, Kc, Vc, sel, p, B)
+            r_prev = row
+            done += 1
+        p += 1
+        if time.perf_counter() - t0 > budget_s:
+            break
+    t_layer_step = (time.perf_counter() - t0) / done
+    step_s = t_layer_step * w.layers * w.batch          # one step of every sequence and layer
+    return {
+        "value": w.batch / step_s,
+        "unit": "tok/s",
+        "cores": int(cores),
+        "kind": "oracle",
+        "sample": (f"one sequence, {layers} layers x {done // layers} steps of the decode workload's "
+                   f"shapes (65536-token caches, b_max {b_max}): {t_layer_step * 1e3:.0f} ms per "
+                   f"(sequence, layer) step, scaled to {w.batch} sequences x {w.layers} layers"),
+    }
+
+
 def run_decode(args, dev) -> dict:
     """Decode workload: batch 16, 65536-token prompt per sequence, 32 layers,
     256 single-token steps, every layer walked. Returns the decode block of
@@ -987,6 +1051,9 @@ def main() -> int:
         torch.cuda.empty_cache()
     if args.only != "prefill" and not args.no_decode:
         out["decode"] = run_decode(args, dev)
+    if "decode" in out and args.only != "decode" and not args.no_cpu_baseline:
+        print("[bench] timing the oracle's decode on the host", file=sys.stderr, flush=True)
+        out["decode"]["cpu_baseline"] = cpu_baseline_decode()
     if cpu_layer is not None and not args.no_cpu_baseline:
         import synth
         w = synth.WORKLOADS["llama8b"]
