@@ -464,6 +464,9 @@ def run_prefill(args, dev):
     achieved = (flops_alg / L) / (attn_ms * 1e-3) / 1e12
 
     value = flops_alg / (ms_per_step * 1e-3) / 1e12
+    # the sketch reads Q and K once: its algorithmic bytes per layer
+    sketch_bytes = (w.h_q + w.h_kv) * int(cu[-1]) * w.d * 2
+    sketch_ms = float(phase[0]) / max(1, min(args.steps, 3)) / L
     out = {
         "metric": "sparse prefill TFLOP/s + decode tok/s at 20% density; sketch+select overhead %",
         "value": round(value, 2),
@@ -487,6 +490,15 @@ def run_prefill(args, dev):
         "executed_tflop_per_step": flops_alg / 1e12,
         "tile_tflop_per_step": flops_tile / 1e12,
         "overhead_pct": round(100.0 * float(phase_frac[:3].sum()), 3),
+        "sketch_hbm": {
+            "call": "sw_sketch_scores (Q/K pooling, FWHT, block scores)",
+            "bytes_per_layer": sketch_bytes,
+            "ms_per_layer": round(sketch_ms, 4),
+            "achieved": round(sketch_bytes / (sketch_ms * 1e-3) / 1e9, 1),
+            "peak": PEAK_HBM_GBS,
+            "unit": "GB/s",
+            "frac": round(sketch_bytes / (sketch_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+        },
         "phase_ms_per_step": {k: round(float(v) / max(1, min(args.steps, 3)), 4)
                               for k, v in zip(("sketch", "walk", "select", "attention"), phase)},
         "roofline": {
