@@ -39,10 +39,10 @@ PEAK_HBM_GBS = 8000.0
 # measured on: a changed source reports null.
 FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
 MEASURED_TRAFFIC = {
-    "attn_prefill.hip": ("ead88101fe94a31d75def7c94fd7fd367a6a5f47365fa53394bf50edc4d109e7",
-                         334305.0 * 1024, 262144.0 * 1024),
+    "attn_prefill.hip": ("2149d18851d90f262dfc6f4961c3e5831781851fa204e37a2fc0bb1999ee0fa0",
+                         334289.8 * 1024, 262144.0 * 1024),
     "attn_decode.hip": ("35298374e364ffeab9cb07588b1482cfc8b2e768beb1ae05288389c6639aa035",
-                        419347.3 * 1024, 1088.0 * 1024),
+                        419327.5 * 1024, 1088.0 * 1024),
 }
 
 
