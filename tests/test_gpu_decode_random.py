@@ -1,0 +1,77 @@
+"""Seeded random configurations of the split-K decode attention against the
+oracle (the kernel given a selection): batches of 1-20 sequences at random
+positions (including inactive ones: negative or past the cache, which get
+zeros), GQA groups 1-8, d in {64, 128}, blocks of 16-128 tokens, bf16 and
+fp32, selections that are random subsets of the blocks up to the current one
+(with or without it), padded with entries the kernel must skip."""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from paper_2602_07397_amd import binding as sw
+
+pytestmark = pytest.mark.gpu
+
+U = pytest.importorskip("_gpu_util")
+
+N_CASES = 16
+
+
+@pytest.mark.parametrize("seed", range(N_CASES))
+def test_random_decode_attention_matches_oracle(seed):
+    rng = np.random.default_rng(2000 + seed)
+    dtype = "f32" if seed % 4 == 3 else "bf16"
+    G = int(rng.choice([1, 2, 4, 8]))
+    h_kv = int(rng.choice([1, 2, 8]))
+    h_q = G * h_kv
+    d = int(rng.choice([64, 128]))
+    B = int(rng.choice([16, 64, 128]))
+    batch = int(rng.integers(1, 21))
+    T_max = int(rng.integers(1, 5000))
+    pos = []
+    for _ in range(batch):
+        u = rng.uniform()
+        pos.append(-1 if u < 0.08 else (T_max + 3 if u < 0.12 else int(rng.integers(0, T_max))))
+    g = torch.Generator().manual_seed(seed)
+    q = torch.randn((batch, h_q, d), generator=g)
+    Kc = torch.randn((batch, h_kv, T_max, d), generator=g)
+    Vc = torch.randn((batch, h_kv, T_max, d), generator=g)
+    td = torch.bfloat16 if dtype == "bf16" else torch.float32
+    q, Kc, Vc = q.to(td), Kc.to(td), Vc.to(td)
+    given, used = [], []
+    for p in pos:
+        if p < 0 or p >= T_max:
+            given.append([0])
+            used.append([])
+            continue
+        bc = p // B
+        keep_cur = rng.uniform() < 0.8
+        s = sorted({j for j in range(bc) if rng.uniform() < rng.uniform(0.1, 0.9)} |
+                   ({bc} if keep_cur or bc == 0 else set()))
+        if not s:
+            s = [bc]
+        gsel = list(s)
+        if seed % 3 == 0:
+            gsel = sorted(gsel + [-1] + [bc + 1 + k for k in range(int(rng.integers(0, 3)))])
+        given.append(gsel)
+        used.append(s)
+    kmax = max(len(s) for s in given)
+    idx = np.full((batch, kmax), -1, dtype=np.int32)
+    cnt = np.zeros(batch, dtype=np.int32)
+    for b, s in enumerate(given):
+        idx[b, :len(s)] = s
+        cnt[b] = len(s)
+    out = sw.sparse_attn_decode(U.to_dev(q), U.to_dev(Kc), U.to_dev(Vc), B,
+                                U.to_dev(np.array(pos, dtype=np.int32)), U.to_dev(idx),
+                                U.to_dev(cnt), kmax)
+    got = out.float().cpu().numpy()
+    tol = U.ATOL_BF16 if dtype == "bf16" else U.ATOL_F32
+    qh, Kh, Vh = O.f64(q), O.f64(Kc), O.f64(Vc)
+    assert np.isfinite(got).all()
+    for b, p in enumerate(pos):
+        if not used[b]:
+            assert np.all(got[b] == 0.0), (seed, b, p)
+            continue
+        ref = O.decode_attention(qh[b], Kh[b], Vh[b], used[b], p, B)
+        assert U.max_abs(got[b], ref) <= tol, (seed, b, p, dtype, G, h_kv, d, B)
