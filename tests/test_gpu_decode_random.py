@@ -75,3 +75,29 @@ def test_random_decode_attention_matches_oracle(seed):
             continue
         ref = O.decode_attention(qh[b], Kh[b], Vh[b], used[b], p, B)
         assert U.max_abs(got[b], ref) <= tol, (seed, b, p, dtype, G, h_kv, d, B)
+
+
+def test_decode_attention_with_every_block_selected_at_max_blocks():
+    """B = 16 with a 65536-token cache: 4096 blocks, every block up to the
+    current one selected (the longest lists the kernel stages)."""
+    rng = np.random.default_rng(3000)
+    batch, h_kv, G, d, B, T_max = 2, 2, 4, 128, 16, 65536
+    h_q = G * h_kv
+    pos = [T_max - 1, int(rng.integers(40000, T_max - 1))]
+    g = torch.Generator().manual_seed(77)
+    q = torch.randn((batch, h_q, d), generator=g).to(torch.bfloat16)
+    Kc = torch.randn((batch, h_kv, T_max, d), generator=g).to(torch.bfloat16)
+    Vc = torch.randn((batch, h_kv, T_max, d), generator=g).to(torch.bfloat16)
+    sels = [list(range(p // B + 1)) for p in pos]
+    kmax = max(len(s) for s in sels)
+    idx = np.full((batch, kmax), -1, dtype=np.int32)
+    cnt = np.array([len(s) for s in sels], dtype=np.int32)
+    for b, s in enumerate(sels):
+        idx[b, :len(s)] = s
+    out = sw.sparse_attn_decode(U.to_dev(q), U.to_dev(Kc), U.to_dev(Vc), B,
+                                U.to_dev(np.array(pos, dtype=np.int32)), U.to_dev(idx),
+                                U.to_dev(cnt), kmax)
+    got = out.float().cpu().numpy()
+    for b, p in enumerate(pos):
+        ref = O.decode_attention(O.f64(q[b]), O.f64(Kc[b]), O.f64(Vc[b]), sels[b], p, B)
+        assert U.max_abs(got[b], ref) <= U.ATOL_BF16, (b, p)
