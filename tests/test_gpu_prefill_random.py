@@ -94,3 +94,31 @@ def test_random_configuration_matches_oracle(seed):
         assert np.isfinite(got[:, a:e]).all(), (seed, s)
         assert U.max_abs(got[:, a:e], ref) <= tol, (seed, s, dtype, B, d, G, mode)
         r += b
+
+
+def test_rows_selecting_every_block_at_max_blocks():
+    """One sequence of SW_MAX_BLOCKS blocks (B = 64): the last rows select
+    every block (the longest lists the kernel compacts in LDS), the others
+    only their diagonal block."""
+    B, d, h_q, h_kv = 64, 64, 2, 1
+    b = sw.MAX_BLOCKS
+    N = b * B
+    g = torch.Generator().manual_seed(91)
+    Q = torch.randn((h_q, N, d), generator=g).to(torch.bfloat16)
+    K = torch.randn((h_kv, N, d), generator=g).to(torch.bfloat16)
+    V = torch.randn((h_kv, N, d), generator=g).to(torch.bfloat16)
+    full = {b - 1, b - 2, b - 5}
+    sel = [list(range(i + 1)) if i in full else [i] for i in range(b)]
+    kmax = b
+    idx = np.full((b, kmax), -1, dtype=np.int32)
+    cnt = np.array([len(s) for s in sel], dtype=np.int32)
+    for r, s in enumerate(sel):
+        idx[r, :len(s)] = s
+    out = sw.sparse_attn_prefill(U.to_dev(Q), U.to_dev(K), U.to_dev(V), [0, N], B, U.to_dev(idx),
+                                 U.to_dev(cnt), kmax)
+    got = out.float().cpu().numpy()
+    Qh, Kh, Vh = O.f64(Q), O.f64(K), O.f64(V)
+    for i in sorted(full) + [0, 1, 1000]:
+        for u in range(h_q):
+            ref = O.sparse_attention_block(Qh, Kh, Vh, B, sel[i], u, i)
+            assert U.max_abs(got[u, i * B:(i + 1) * B], ref) <= U.ATOL_BF16, (i, u)
