@@ -44,7 +44,7 @@ def test_sketch_matches_oracle_fp32(n):
     assert sk["A_scale"].item() == pytest.approx(ref["c"], rel=1e-12)
 
 
-@pytest.mark.parametrize("B,d", [(128, 128), (64, 128), (64, 64), (16, 32)])
+@pytest.mark.parametrize("B,d", [(128, 128), (64, 128), (64, 64), (16, 32), (32, 256), (16, 16)])
 def test_sketch_matches_oracle_bf16_gqa_varlen(B, d):
     w = _bf16_case((1000, 384, 257, 64), d=d, B=B)
     Q, K, _ = synth.prefill_layer_inputs(w, 0)
