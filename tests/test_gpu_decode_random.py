@@ -101,3 +101,45 @@ def test_decode_attention_with_every_block_selected_at_max_blocks():
     for b, p in enumerate(pos):
         ref = O.decode_attention(O.f64(q[b]), O.f64(Kc[b]), O.f64(Vc[b]), sels[b], p, B)
         assert U.max_abs(got[b], ref) <= U.ATOL_BF16, (b, p)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_decode_attention_large_logits_and_identical_keys(dtype):
+    """Logits of several hundred (far past the fp32 exp range without a
+    running max) and, in the second sequence, identical keys (uniform
+    weights: the output is the mean of the selected values up to p)."""
+    batch, h_kv, G, d, B, T_max = 2, 1, 4, 128, 64, 3000
+    h_q = G * h_kv
+    g = torch.Generator().manual_seed(5)
+    q = torch.randn((batch, h_q, d), generator=g) * 12.0
+    Kc = torch.randn((batch, h_kv, T_max, d), generator=g) * 12.0
+    Vc = torch.randn((batch, h_kv, T_max, d), generator=g)
+    Kc[1] = 0.25
+    td = torch.bfloat16 if dtype == "bf16" else torch.float32
+    q, Kc, Vc = q.to(td), Kc.to(td), Vc.to(td)
+    pos = [2999, 1500]
+    sels = [[0, 5, 17, 30, 46], [0, 3, 10, 23]]
+    kmax = 5
+    idx = np.full((batch, kmax), -1, dtype=np.int32)
+    cnt = np.array([len(s) for s in sels], dtype=np.int32)
+    for b, s in enumerate(sels):
+        idx[b, :len(s)] = s
+    out = sw.sparse_attn_decode(U.to_dev(q), U.to_dev(Kc), U.to_dev(Vc), B,
+                                U.to_dev(np.array(pos, dtype=np.int32)), U.to_dev(idx),
+                                U.to_dev(cnt), kmax)
+    got = out.float().cpu().numpy()
+    assert np.isfinite(got).all()
+    qh, Kh, Vh = O.f64(q), O.f64(Kc), O.f64(Vc)
+    ref0 = O.decode_attention(qh[0], Kh[0], Vh[0], sels[0], pos[0], B)
+    # fp32: forward error bound of the logits (gamma_d sum|q_i k_i| plus a
+    # few ulps of |z| for the scaling and exponential); a logit perturbation
+    # of at most delta moves the output by at most (e^(2 delta) - 1) max|V|
+    u = 2.0 ** -24
+    dots = float((np.abs(qh[0]) @ np.abs(Kh[0, 0]).T).max()) / np.sqrt(d)
+    delta = (d * u / (1 - d * u)) * dots + 4 * u * dots
+    tol0 = U.ATOL_BF16 if dtype == "bf16" else np.expm1(2 * delta) * float(np.abs(Vh[0]).max()) + U.ATOL_F32
+    assert U.max_abs(got[0], ref0) <= tol0
+    toks = np.concatenate([np.arange(j * B, min(pos[1] + 1, (j + 1) * B)) for j in sels[1]])
+    mean = Vh[1, 0, toks].mean(axis=0)
+    for u in range(h_q):
+        assert U.max_abs(got[1, u], mean) <= (U.ATOL_BF16 if dtype == "bf16" else U.ATOL_F32)
