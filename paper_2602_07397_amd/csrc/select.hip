@@ -22,7 +22,7 @@ __device__ __forceinline__ int row_budget_dev(int avail, int nf, int k, int pct)
 }
 
 // Selects from vals[0..avail) with forced set {first, last} (-1 = none).
-__device__ void select_row_dev(const double* __restrict__ vals, int avail, int first, int last,
+__device__ __forceinline__ void select_row_dev(const double* __restrict__ vals, int avail, int first, int last,
                                int k, int pct, int32_t* __restrict__ out, int32_t* __restrict__ cnt,
                                int kmax) {
   __shared__ int hist[256];
