@@ -64,19 +64,28 @@ __device__ __forceinline__ unsigned long long order_key(double v) {
   return (u >> 63) ? ~u : (u | 0x8000000000000000ull);
 }
 
+// Inclusive prefix sum over the 64 lanes of a wavefront with DPP moves:
+// shifts by 1, 2, 4 and 8 lanes within each 16-lane row (lanes without a
+// source add 0), then lane 15 of each row added to the next row and lane 31
+// to the upper half.
+__device__ __forceinline__ int wave_inclusive_scan(int x) {
+  x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xf, 0xf, true);   // row_shr:1
+  x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xf, 0xf, true);   // row_shr:2
+  x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xf, 0xf, true);   // row_shr:4
+  x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xf, 0xf, true);   // row_shr:8
+  x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xa, 0xf, false);  // row_bcast:15, rows 1 and 3
+  x += __builtin_amdgcn_update_dpp(0, x, 0x143, 0xc, 0xf, false);  // row_bcast:31, rows 2 and 3
+  return x;
+}
+
 // Exclusive prefix sum over a 256-thread block (4 wavefronts): an inclusive
-// scan inside each wavefront by lane shuffles, then the wavefront totals
+// scan inside each wavefront (DPP moves), then the wavefront totals
 // through LDS. `tmp` holds at least 4 ints of LDS. Returns the exclusive
 // prefix of `v`; `*total` receives the block sum. Contains two barriers.
 __device__ __forceinline__ int block_exclusive_scan_256(int v, int* tmp, int* total) {
   const int t = threadIdx.x;
   const int lane = t & 63, w = t >> 6;
-  int x = v;
-#pragma unroll
-  for (int off = 1; off < 64; off <<= 1) {
-    const int y = __shfl_up(x, off);
-    if (lane >= off) x += y;
-  }
+  const int x = wave_inclusive_scan(v);
   if (lane == 63) tmp[w] = x;
   __syncthreads();
   int before = 0;
