@@ -17,6 +17,26 @@
 namespace sw {
 
 constexpr float kLog2eD = 1.4426950408889634f;
+
+// Combine a lane's value with that of lane ^ 16 / lane ^ 32 through the
+// permlane swaps (VALU moves; each returns the lane's own value and its
+// partner's in some order).
+__device__ __forceinline__ float fmax_xor16(float v) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float fmax_xor32(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float sum_xor16(float v) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float sum_xor32(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
 constexpr int kDecodeSelCache = 512;   // selected-block entries cached per workgroup
 
 // Tuning constants (overridable at build time).
@@ -392,8 +412,8 @@ __global__ __launch_bounds__(256) void attn_decode_mfma_kernel(
         sv[v] = (key <= p) ? sacc[v] * sl2 : -INFINITY;
         mx = fmaxf(mx, sv[v]);
       }
-      mx = fmaxf(mx, __shfl_xor(mx, 16));
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      mx = fmax_xor16(mx);
+      mx = fmax_xor32(mx);
       const float mnew = fmaxf(mrun, mx);          // finite: key tok0 <= p is valid
       const float alpha = exp2f(mrun - mnew);
       mrun = mnew;
@@ -436,8 +456,8 @@ __global__ __launch_bounds__(256) void attn_decode_mfma_kernel(
   __syncthreads();                                 // V^T slices are dead from here
   // per-wave partials: head ln; lane groups hold disjoint keys (sum l) and
   // disjoint output dims
-  float lsum = lrun + __shfl_xor(lrun, 16);
-  lsum += __shfl_xor(lsum, 32);
+  float lsum = sum_xor16(lrun);
+  lsum = sum_xor32(lsum);
   if (lg == 0) {
     sm_m[w][ln] = mrun;
     sm_l[w][ln] = lsum;
