@@ -40,9 +40,9 @@ PEAK_HBM_GBS = 8000.0
 FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
 MEASURED_TRAFFIC = {
     "attn_prefill.hip": ("2149d18851d90f262dfc6f4961c3e5831781851fa204e37a2fc0bb1999ee0fa0",
-                         334289.8 * 1024, 262144.0 * 1024),
-    "attn_decode.hip": ("35298374e364ffeab9cb07588b1482cfc8b2e768beb1ae05288389c6639aa035",
-                        419327.5 * 1024, 1088.0 * 1024),
+                         334278.8 * 1024, 262144.0 * 1024),
+    "attn_decode.hip": ("e75a2c49d4006ba95d386c0e789150059e2b98497164fdcd8ce9320dd90b1790",
+                        419752.1 * 1024, 1088.0 * 1024),
 }
 
 
