@@ -311,7 +311,8 @@ int64_t sw_decode_attn_workspace_bytes(int batch, int h_q, int h_kv, int d);
  * t <= pos[b] of the selected blocks, applied to Vc. Split-K over the
  * selected tokens with a log-sum-exp merge. q [batch][h_q][d]; Kc, Vc
  * [batch][h_kv][T_max][d]; O [batch][h_q][d] in the input dtype.
- * G = h_q / h_kv in {1, 2, 4, 8}; d in {64, 128}; scale <= 0 -> 1/sqrt(d).
+ * G = h_q / h_kv in {1, 2, 4, 8}; d in {64, 128}; B a multiple of 16 in
+ * [16, 1024] (SW_ERR_INVALID_ARG otherwise); scale <= 0 -> 1/sqrt(d).
  */
 int sw_sparse_attn_decode(int dtype, const void* q, const void* Kc, const void* Vc, int batch,
                           int h_q, int h_kv, int d, int T_max, int B, const int32_t* pos,

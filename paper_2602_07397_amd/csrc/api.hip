@@ -452,7 +452,9 @@ int sw_sparse_attn_decode(int dtype, const void* q, const void* Kc, const void* 
   if (d != 64 && d != 128) return fail(SW_ERR_UNSUPPORTED, "decode attention head dim d=%d (64 or 128)", d);
   if (batch < 1 || batch > 65536) return fail(SW_ERR_INVALID_ARG, "batch=%d", batch);
   if (T_max < 1) return fail(SW_ERR_INVALID_ARG, "T_max=%d", T_max);
-  if (B < 1 || B > 1024) return fail(SW_ERR_INVALID_ARG, "B=%d", B);
+  // the kernels walk a selected block in 16-token groups
+  if (B < 16 || B > 1024 || B % 16 != 0)
+    return fail(SW_ERR_INVALID_ARG, "B=%d must be a multiple of 16 in [16, 1024]", B);
   if (kmax < 1) return fail(SW_ERR_INVALID_ARG, "kmax=%d < 1", kmax);
   CHECK(check_ptr(q, 16, "q"));
   CHECK(check_ptr(Kc, 16, "Kc"));

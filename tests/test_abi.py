@@ -117,6 +117,16 @@ def test_walk_select_attention_reject_bad_arguments():
     assert rc == 1
 
 
+@pytest.mark.parametrize("B", [0, 8, 40, 1040])
+def test_decode_attention_rejects_block_sizes_off_the_16_token_grid(B):
+    """The decode attention walks each selected block in 16-token groups: a
+    block size that is not a multiple of 16 in [16, 1024] is refused before
+    anything is enqueued."""
+    rc, msg = _err("sw_sparse_attn_decode", sw.SW_BF16, FAKE, FAKE, FAKE, 2, 8, 2, 128, 4096, B,
+                   FAKE, FAKE, FAKE, 8, ctypes.c_float(0.0), FAKE, FAKE, 1 << 30, None)
+    assert rc == 1 and "B=" in msg, msg
+
+
 def test_binding_refuses_cpu_tensors():
     import torch
     x = torch.zeros((1, 64, 64))
