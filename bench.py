@@ -166,7 +166,9 @@ def cpu_baseline_decode(budget_s: float = 10.0, layers: int = 4, seed: int = 0) 
         qbar[:b0] = rng.standard_normal((b0, d))
         kbar[:b0] = rng.standard_normal((b0, d))
         last = n0 - (b0 - 1) * B
-        states.append(O.DecodeLayerState(qbar, kbar, last, last, A, float(np.abs(A).max())))
+        qtok = rng.standard_normal((last, d))
+        ktok = rng.standard_normal((last, d))
+        states.append(O.DecodeLayerState(qbar, kbar, qtok, ktok, A, float(np.abs(A).max())))
     Kc = rng.standard_normal((w.h_kv, T, d))
     Vc = rng.standard_normal((w.h_kv, T, d))
     t0 = time.perf_counter()

@@ -424,25 +424,26 @@ def prefill_layer(Q, K, V, B: int, signs, cols, s: int, R_prev: Optional[np.ndar
 
 @dataclasses.dataclass
 class DecodeLayerState:
-    """Per-(sequence, layer) caches Alg. 2 carries between steps: block
-    representatives with the token count of the open block, the score
-    matrix A (b_max x b_max) and the prefill score scale c."""
+    """Per-(sequence, layer) caches Alg. 2 carries between steps: the block
+    representatives (means of closed blocks), the head-averaged query and key
+    of every token of the open block so far, the score matrix A
+    (b_max x b_max) and the prefill score scale c."""
     qbar: np.ndarray
     kbar: np.ndarray
-    qcnt: int
-    kcnt: int
+    qtok: np.ndarray      # [tokens of the open block][d], head-averaged queries
+    ktok: np.ndarray      # [tokens of the open block][d], head-averaged keys
     A: np.ndarray
     c: float
 
     def copy(self) -> "DecodeLayerState":
-        return DecodeLayerState(self.qbar.copy(), self.kbar.copy(), self.qcnt,
-                                self.kcnt, self.A.copy(), self.c)
+        return DecodeLayerState(self.qbar.copy(), self.kbar.copy(), self.qtok.copy(),
+                                self.ktok.copy(), self.A.copy(), self.c)
 
 
 def decode_state_from_prefill(Q, K, B: int, signs, cols, b_max: int) -> DecodeLayerState:
     """Caches Alg. 2 takes over from the prefill of an n-token prompt: block
-    means (the last, possibly partial, block with its count), the prefill
-    score matrix and its scale."""
+    means, the head-averaged tokens of the last (possibly partial) block, the
+    prefill score matrix and its scale."""
     sk = sketch_scores(Q, K, B, signs, cols)
     n = f64(Q).shape[1]
     b = sk["qbar"].shape[0]
@@ -453,8 +454,10 @@ def decode_state_from_prefill(Q, K, B: int, signs, cols, b_max: int) -> DecodeLa
     kbar[:b] = sk["kbar"]
     A = np.zeros((b_max, b_max))
     A[:b, :b] = sk["A"]
-    last = n - (b - 1) * B
-    return DecodeLayerState(qbar, kbar, last, last, A, sk["c"])
+    first = (b - 1) * B                      # first token of the last block
+    qtok = head_mean(f64(Q)[:, first:n])
+    ktok = head_mean(f64(K)[:, first:n])
+    return DecodeLayerState(qbar, kbar, qtok, ktok, A, sk["c"])
 
 
 def decode_layer_step(st: DecodeLayerState, q_new, k_new, p: int, r_prev: Optional[np.ndarray],
@@ -462,27 +465,26 @@ def decode_layer_step(st: DecodeLayerState, q_new, k_new, p: int, r_prev: Option
                       flags: int = FORCE_BOTH, variant: int = WALK_POWER):
     """Alg. 2 steps 2-6 for the token at 0-based position p of one sequence
     at one layer. q_new [h_q][d], k_new [h_kv][d]. Updates ``st`` in place and
-    returns (walk row over key blocks 0..b_cur, selected blocks, gap)."""
+    returns (walk row over key blocks 0..b_cur, selected blocks, gap).
+
+    The open block's representatives are the token-space sketch itself (the
+    mean over the tokens the block holds so far, Sec. 2.2), recomputed from
+    its tokens; Alg. 2's running-mean update gives the same value."""
     q_new, k_new = f64(q_new), f64(k_new)
     b_cur = p // B
     b_q = b_cur
     r = len(cols)
-    # step 2: running mean of the open key block's representative
-    k_avg = k_new.sum(axis=0) / k_new.shape[0]
+    # steps 2-3: the new token joins the open block (a block starts at p % B == 0)
+    q_avg = head_mean(q_new[:, None, :])[0]
+    k_avg = head_mean(k_new[:, None, :])[0]
     if p % B == 0:
-        st.kbar[b_cur] = k_avg
-        st.kcnt = 1
+        st.qtok = q_avg[None, :]
+        st.ktok = k_avg[None, :]
     else:
-        st.kbar[b_cur] = (st.kcnt * st.kbar[b_cur] + k_avg) / (st.kcnt + 1)
-        st.kcnt += 1
-    # step 3: head-averaged query (its block representative kept the same way)
-    q_avg = q_new.sum(axis=0) / q_new.shape[0]
-    if p % B == 0:
-        st.qbar[b_q] = q_avg
-        st.qcnt = 1
-    else:
-        st.qbar[b_q] = (st.qcnt * st.qbar[b_q] + q_avg) / (st.qcnt + 1)
-        st.qcnt += 1
+        st.qtok = np.concatenate([st.qtok, q_avg[None, :]])
+        st.ktok = np.concatenate([st.ktok, k_avg[None, :]])
+    st.kbar[b_cur] = block_means(st.ktok, B)[0]
+    st.qbar[b_q] = block_means(st.qtok, B)[0]
     q_t = srht(q_avg[None, :], signs, cols)[0]
     Ks = srht(st.kbar[:b_cur + 1], signs, cols)
     Qs = srht(st.qbar[:b_q + 1], signs, cols)

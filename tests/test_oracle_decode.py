@@ -36,7 +36,7 @@ def _run(env, p_from, p_to, states, pct=40):
     return out
 
 
-def test_running_mean_equals_block_mean():
+def test_open_block_mean_equals_block_mean():
     env = _setup()
     _run(env, env["n0"], env["T"], env["states"])
     B, T = env["B"], env["T"]
@@ -45,7 +45,7 @@ def test_running_mean_equals_block_mean():
         qb = O.block_means(O.head_mean(env["Q"][l][:, :T]), B)
         np.testing.assert_allclose(st.kbar[:kb.shape[0]], kb, rtol=1e-12, atol=1e-13)
         np.testing.assert_allclose(st.qbar[:qb.shape[0]], qb, rtol=1e-12, atol=1e-13)
-        assert st.kcnt == T - (kb.shape[0] - 1) * B
+        assert st.ktok.shape[0] == st.qtok.shape[0] == T - (kb.shape[0] - 1) * B
 
 
 def test_score_row_and_column_follow_their_definitions():
@@ -121,3 +121,35 @@ def test_state_round_trip_is_bit_identical():
         for (rx, sx), (ry, sy) in zip(x, y):
             assert sx == sy
             np.testing.assert_array_equal(rx, ry)
+
+
+def test_state_from_prefill_places_the_prompt_scores():
+    """The decode caches taken over from an n-token prompt (n not a multiple
+    of B): at r = d the score cache holds the Sec. 2.1 block score (the
+    literal double sum over token pairs divided by sqrt(d)) at (i, j) for
+    j <= i < b, zero everywhere else of the b_max x b_max cache; the block
+    representatives are the per-block token means and the open block's token
+    list holds the head-averaged tokens of the prompt's last block."""
+    rng = np.random.default_rng(11)
+    h_q, h_kv, d, B, n, b_max = 4, 2, 8, 4, 18, 9
+    Q = rng.normal(size=(h_q, n, d))
+    K = rng.normal(size=(h_kv, n, d))
+    signs = rng.choice([-1, 1], size=d)
+    cols = rng.permutation(d)
+    st = O.decode_state_from_prefill(Q, K, B, signs, cols, b_max)
+    b = -(-n // B)
+    Qa = np.array([[sum(Q[u, t, e] for u in range(h_q)) / h_q for e in range(d)] for t in range(n)])
+    Ka = np.array([[sum(K[g, t, e] for g in range(h_kv)) / h_kv for e in range(d)] for t in range(n)])
+    want = np.zeros((b_max, b_max))
+    for i in range(b):
+        for j in range(i + 1):
+            want[i, j] = O.block_score_true(Qa, Ka, B, i, j)
+    np.testing.assert_allclose(st.A, want, rtol=1e-12, atol=1e-13)
+    assert st.c == pytest.approx(np.max(np.abs(want)), rel=1e-12)
+    for i in range(b):
+        lo, hi = i * B, min(n, (i + 1) * B)
+        np.testing.assert_allclose(st.qbar[i], Qa[lo:hi].mean(axis=0), rtol=1e-12, atol=1e-14)
+        np.testing.assert_allclose(st.kbar[i], Ka[lo:hi].mean(axis=0), rtol=1e-12, atol=1e-14)
+    assert not st.qbar[b:].any() and not st.kbar[b:].any()
+    np.testing.assert_allclose(st.qtok, Qa[(b - 1) * B:], rtol=1e-12, atol=1e-14)
+    np.testing.assert_allclose(st.ktok, Ka[(b - 1) * B:], rtol=1e-12, atol=1e-14)
