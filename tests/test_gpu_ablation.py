@@ -27,3 +27,68 @@ def test_ablation_runs_and_is_bounded(data):
             assert r["selected_fraction"] == pytest.approx(1.0)
         if data == "planted":
             assert r["needle_recall"] is not None
+
+
+CHECKED = [("default", "-"), ("r", 16), ("r", 128), ("s", 1), ("s", 4), ("s", 16), ("pct", 10),
+           ("walk", "off"), ("walk_layers", 2), ("variant", "relu_power"),
+           ("variant", "row_softmax")]
+
+
+def test_ablation_selections_match_the_oracle():
+    """The harness's own selections (sketch dimensions 16 and 128, exponents
+    1, 4 and 16, 10 % density, the walk off or restarted every 2 layers, the
+    clipped-power and row-softmax transitions, and the default) against the
+    oracle's walk and selection on the same inputs: exact on every row whose
+    gap exceeds the tie tolerance. (The matrix-power transition has its own
+    forward-error-bound test.)"""
+    import math
+
+    import numpy as np
+    import oracle as O
+    import synth
+    from paper_2602_07397_amd import binding as sw
+
+    U = pytest.importorskip("_gpu_util")
+    dev = torch.device("cuda:0")
+    args = argparse.Namespace(ablation_tokens=4096, ablation_layers=4, ablation_needles=6,
+                              ablation_data="topics", ablation_drift=0.1)
+    record = {}
+    bench.run_ablation(args, dev, record=record)
+    w = synth.scaled(synth.WORKLOADS["llama8b"], seqlens=(args.ablation_tokens,),
+                     layers=args.ablation_layers, needles=args.ablation_needles)
+    variants = {"power": O.WALK_POWER, "relu_power": O.WALK_RELU, "row_softmax": O.WALK_SOFTMAX}
+    settings = {}
+    for axis, value in CHECKED:
+        c = dict(r=64, s=8, pct=20, window=0, walk=True, variant="power")
+        if axis in ("r", "s", "pct"):
+            c[axis] = value
+        elif axis == "walk":
+            c["walk"] = False
+        elif axis == "walk_layers":
+            c["window"] = value
+        elif axis == "variant":
+            c["variant"] = value
+        settings[(axis, value)] = c
+    state = {key: None for key in settings}
+    near, rows = 0, 0
+    for layer in range(w.layers):
+        Q, K, _ = synth.topic_layer_inputs(w, layer, device=dev, drift=args.ablation_drift)
+        Qh, Kh = Q.cpu(), K.cpu()
+        sketches = {}
+        for key, c in settings.items():
+            r = c["r"]
+            if r not in sketches:
+                signs, cols = synth.srht_params(w.d, r, w.seed)
+                sketches[r] = O.sketch_scores(Qh, Kh, w.B, signs, cols)
+            sk = sketches[r]
+            restart = (not c["walk"]) or (c["window"] > 0 and layer % c["window"] == 0)
+            W = O.walk_weights_variant(variants[c["variant"]], sk["A"], sk["c"], c["s"],
+                                       logit_scale=math.sqrt(r / w.d))
+            R = O.walk_step(None if restart else state[key], W)
+            state[key] = R
+            sel, gaps = O.select_blocks(R, pct=c["pct"])
+            idx, cnt = record[(key[0], key[1], layer)]
+            got = [idx[i, :cnt[i]].tolist() for i in range(idx.shape[0])]
+            near += U.check_selection(got, sel, gaps, R)
+            rows += len(got)
+    assert near <= 0.05 * rows, (near, rows)

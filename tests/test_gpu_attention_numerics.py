@@ -49,6 +49,14 @@ def _f32_bound(Q, K, V, scale=None):
     return math.expm1(2 * delta) * float(Vh.max()) + U.ATOL_F32
 
 
+def _f32_tol(Q, K, V, cap):
+    """The fp32 tolerance where the logits reach hundreds: the worst-case
+    bound above, capped at `cap`, a fixed ceiling a few times the error the
+    kernel shows on these inputs, so that a rescaling mistake well inside the
+    (loose) worst-case bound still fails."""
+    return min(_f32_bound(Q, K, V), cap)
+
+
 def _inputs(n, h_q, h_kv, d, seed, kscale=None):
     g = torch.Generator().manual_seed(seed)
     Q = torch.randn((h_q, n, d), generator=g)
@@ -73,9 +81,12 @@ def test_growing_scores_force_reference_fixups(dtype, B):
     out, lse = sw.sparse_attn_prefill(U.to_dev(Q), U.to_dev(K), U.to_dev(V), [0, n], B, idx, cnt,
                                       kmax, want_lse=True)
     ref = O.sparse_attention_prefill(Q, K, V, B, sel)
-    tol = U.ATOL_BF16 if dtype == "bf16" else _f32_bound(Q, K, V)
+    # fp32: logits up to ~300; observed max-abs error 1.9e-5
+    tol = U.ATOL_BF16 if dtype == "bf16" else _f32_tol(Q, K, V, 5e-5)
     assert torch.isfinite(out.float()).all() and torch.isfinite(lse).all()
-    assert U.max_abs(out.float().cpu().numpy(), ref) <= tol
+    err = U.max_abs(out.float().cpu().numpy(), ref)
+    print(f"\n[numerics] growing scores {dtype} B={B}: max-abs {err:.2e}, tolerance {tol:.2e}")
+    assert err <= tol
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
@@ -93,9 +104,12 @@ def test_large_logits_stay_finite(dtype):
     idx, cnt, kmax = _pack(sel)
     out = sw.sparse_attn_prefill(U.to_dev(Q), U.to_dev(K), U.to_dev(V), [0, n], B, idx, cnt, kmax)
     ref = O.sparse_attention_prefill(Q, K, V, B, sel)
-    tol = U.ATOL_BF16 if dtype == "bf16" else _f32_bound(Q, K, V)
+    # fp32: logits of several hundred; observed max-abs error 1.2e-4
+    tol = U.ATOL_BF16 if dtype == "bf16" else _f32_tol(Q, K, V, 3e-4)
     assert torch.isfinite(out.float()).all()
-    assert U.max_abs(out.float().cpu().numpy(), ref) <= tol
+    err = U.max_abs(out.float().cpu().numpy(), ref)
+    print(f"\n[numerics] large logits {dtype}: max-abs {err:.2e}, tolerance {tol:.2e}")
+    assert err <= tol
 
 
 def test_identical_keys_give_uniform_weights():

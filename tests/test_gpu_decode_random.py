@@ -131,14 +131,12 @@ def test_decode_attention_large_logits_and_identical_keys(dtype):
     assert np.isfinite(got).all()
     qh, Kh, Vh = O.f64(q), O.f64(Kc), O.f64(Vc)
     ref0 = O.decode_attention(qh[0], Kh[0], Vh[0], sels[0], pos[0], B)
-    # fp32: forward error bound of the logits (gamma_d sum|q_i k_i| plus a
-    # few ulps of |z| for the scaling and exponential); a logit perturbation
-    # of at most delta moves the output by at most (e^(2 delta) - 1) max|V|
-    u = 2.0 ** -24
-    dots = float((np.abs(qh[0]) @ np.abs(Kh[0, 0]).T).max()) / np.sqrt(d)
-    delta = (d * u / (1 - d * u)) * dots + 4 * u * dots
-    tol0 = U.ATOL_BF16 if dtype == "bf16" else np.expm1(2 * delta) * float(np.abs(Vh[0]).max()) + U.ATOL_F32
-    assert U.max_abs(got[0], ref0) <= tol0
+    # fp32: the logits reach several hundred, but the split-K kernel keeps the
+    # error (observed 3.6e-6) within the general fp32 tolerance
+    tol0 = U.ATOL_BF16 if dtype == "bf16" else U.ATOL_F32
+    err0 = U.max_abs(got[0], ref0)
+    print(f"\n[numerics] decode large logits {dtype}: max-abs {err0:.2e}, tolerance {tol0:.2e}")
+    assert err0 <= tol0
     toks = np.concatenate([np.arange(j * B, min(pos[1] + 1, (j + 1) * B)) for j in sels[1]])
     mean = Vh[1, 0, toks].mean(axis=0)
     for u in range(h_q):

@@ -38,30 +38,50 @@ def _to_host(*ts):
     return [O.f64(t) for t in ts]
 
 
+def _head_block_error(Q, K, V, Og, B, G, sel_row, u, i):
+    """Oracle rows of query block i for head u (one query head and its KV
+    head, tokens up to the end of the block) against the GPU's output."""
+    g = u // G
+    lo, hi = i * B, min(Q.shape[1], (i + 1) * B)
+    ref = O.sparse_attention_block(O.f64(Q[u:u + 1, :hi].cpu()), O.f64(K[g:g + 1, :hi].cpu()),
+                                   O.f64(V[g:g + 1, :hi].cpu()), B, sel_row, 0, i)
+    return U.max_abs(Og[u, lo:hi].float().cpu().numpy(), ref)
+
+
 def test_llama8b_layers_full_size():
-    """Llama-3-8B-shaped prefill (32/8 heads, d=128, n=32768, B=128, 20%),
-    8 consecutive walked layers."""
+    """Llama-3-8B-shaped prefill (32/8 heads, d=128, n=32768, B=128, 20%):
+    all 32 walked layers, every selection row of every layer checked against
+    the oracle's walk, and sampled (head, query block) attention outputs of
+    every layer."""
     w = synth.WORKLOADS["llama8b"]
     signs, cols, ts, tc = U.srht_dev(w.d, w.r, w.seed)
     cu = synth.cu_seqlens(w.seqlens)
     rng = np.random.default_rng(7)
+    G = w.h_q // w.h_kv
     R_gpu, R_ref = None, None
     near_total, rows_total, worst = 0, 0, 0.0
-    for layer in range(8):
+    per_layer = []
+    for layer in range(w.layers):
         Q, K, V = synth.prefill_layer_inputs(w, layer, device=U.DEV)
         res = U.gpu_prefill_layer(Q, K, V, cu, w.B, ts, tc, w.s, R_gpu, pct=w.pct)
         R_gpu = res["R"]
-        Qh, Kh, Vh = _to_host(Q, K, V)
-        ref = O.prefill_layer(Qh, Kh, Vh, w.B, signs, cols, w.s, R_ref, pct=w.pct, attention=False)
+        ref = O.prefill_layer(Q.cpu(), K.cpu(), None, w.B, signs, cols, w.s, R_ref, pct=w.pct,
+                              attention=False)
         R_ref = ref["R"]
         got = U.gpu_selection(res["idx"], res["cnt"])
-        near_total += U.check_selection(got, ref["sel"], ref["gaps"], R_ref)
+        near = U.check_selection(got, ref["sel"], ref["gaps"], R_ref)
+        near_total += near
         rows_total += len(got)
         b = len(got)
-        pairs = [(int(rng.integers(w.h_q)), i) for i in _sample_blocks(b, rng, 5)]
-        Og = res["O"].float().cpu().numpy()
-        worst = max(worst, _check_attention_sample(Qh, Kh, Vh, Og, w.B, got, pairs))
-        del Qh, Kh, Vh, Og
+        err = 0.0
+        for i in _sample_blocks(b, rng, 3):
+            u = int(rng.integers(w.h_q))
+            err = max(err, _head_block_error(Q, K, V, res["O"], w.B, G, got[i], u, i))
+        worst = max(worst, err)
+        per_layer.append((near, err))
+        del Q, K, V, res
+    print("\n[depth] llama8b near-tie rows / attention max-abs per layer: "
+          + " ".join(f"{n}/{e:.1e}" for n, e in per_layer))
     assert worst <= U.ATOL_BF16, worst
     assert near_total <= 0.05 * rows_total, (near_total, rows_total)
 
