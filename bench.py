@@ -888,17 +888,22 @@ def best_mask(M, pct: int):
     return torch.from_numpy(mask).to(M.device)
 
 
-def run_ablation(args, dev) -> dict:
+def run_ablation(args, dev, record=None) -> dict:
     """Recall of the block selection on synthetic data, one factor
     at a time around the default (r = 64, s = 8, 20 %, walk across layers,
     element-wise power): the sketch dimension r, the exponent s, the density,
-    the cross-layer walk (off = each layer ranks its own W), and the walk
-    transition. Two measures per configuration, averaged over layers:
+    the cross-layer walk (off = each layer ranks its own W; "walk_layers" k =
+    the walk restarts every k layers, so it accumulates at most k layers),
+    and the walk transition. Two measures per configuration, averaged over
+    layers:
     mass recall = the share of the dense attention mass (all query heads)
     that the selected blocks hold; needle recall = the share of planted
     needle blocks selected for the query block that holds the needle's
     query. "best" rows select by the true mass itself (an upper bound at
-    each density)."""
+    each density). The default configuration's recall is also reported per
+    layer (after 1, 2, ... walked layers). ``record``, if a dict, receives
+    every configuration's selection per layer: record[(axis, value, layer)]
+    = (idx, cnt) on the host."""
     import torch
     import synth
     from paper_2602_07397_amd import binding as sw
@@ -908,7 +913,7 @@ def run_ablation(args, dev) -> dict:
     n, B, d = w.seqlens[0], w.B, w.d
     b = -(-n // B)
     cu = synth.cu_seqlens(w.seqlens)
-    base = dict(r=64, s=8, pct=20, walk=True, variant=sw.WALK_POWER)
+    base = dict(r=64, s=8, pct=20, walk=True, window=0, variant=sw.WALK_POWER)
     names = {sw.WALK_POWER: "power", sw.WALK_RELU: "relu_power", sw.WALK_SOFTMAX: "row_softmax",
              sw.WALK_MATPOW: "matrix_power"}
     configs = [("default", "-", dict(base))]
@@ -919,6 +924,9 @@ def run_ablation(args, dev) -> dict:
     for pct in (10, 30, 50, 100):
         configs.append(("pct", pct, dict(base, pct=pct)))
     configs.append(("walk", "off", dict(base, walk=False)))
+    for k in (2, 4):
+        if k < w.layers:
+            configs.append(("walk_layers", k, dict(base, window=k)))
     for v in (sw.WALK_RELU, sw.WALK_SOFTMAX, sw.WALK_MATPOW):
         configs.append(("variant", names[v], dict(base, variant=v)))
     rs = sorted({c["r"] for _, _, c in configs})
@@ -930,6 +938,7 @@ def run_ablation(args, dev) -> dict:
     acc = [dict(mass=0.0, needle_hits=0, needles=0, density=0.0) for _ in configs]
     best = {p: dict(mass=0.0, needle_hits=0, needles=0) for p in sorted({c["pct"] for _, _, c in configs})}
     causal_pairs = b * (b + 1) / 2
+    depth = []                       # the default configuration's recall per layer
     t0 = time.perf_counter()
     for layer in range(w.layers):
         if args.ablation_data == "topics":
@@ -945,14 +954,20 @@ def run_ablation(args, dev) -> dict:
         del Q, K
         for ci, (_, _, c) in enumerate(configs):
             sk = sks[c["r"]]
+            restart = (not c["walk"]) or (c["window"] > 0 and layer % c["window"] == 0)
             R = sw.walk_update_variant(c["variant"], sk["A"], sk["A_scale"], c["s"], cu, B,
-                                       state[ci] if c["walk"] else None,
+                                       None if restart else state[ci],
                                        logit_scale=math.sqrt(c["r"] / d))
             state[ci] = R
             idx, cnt, _ = sw.select_topk_blocks(R, cu, B, density_pct=c["pct"])
+            if record is not None:
+                record[(configs[ci][0], configs[ci][1], layer)] = (idx.cpu(), cnt.cpu())
             mask = selection_mask(idx, cnt, b)
             a = acc[ci]
-            a["mass"] += float((M * mask).sum(dim=1).mean())
+            m_layer = float((M * mask).sum(dim=1).mean())
+            a["mass"] += m_layer
+            if ci == 0:
+                depth.append(round(m_layer, 4))
             a["density"] += float(cnt.sum()) / causal_pairs
             a["best_overlap"] = a.get("best_overlap", 0.0) + float(
                 (mask & best_masks[c["pct"]]).sum()) / float(best_masks[c["pct"]].sum())
@@ -973,7 +988,8 @@ def run_ablation(args, dev) -> dict:
     rows = []
     for (axis, value, c), a in zip(configs, acc):
         rows.append({"axis": axis, "value": value, "r": c["r"], "s": c["s"], "pct": c["pct"],
-                     "walk": c["walk"], "variant": names[c["variant"]],
+                     "walk": c["walk"], "walk_layers": c["window"] or (L if c["walk"] else 1),
+                     "variant": names[c["variant"]],
                      "mass_recall": round(a["mass"] / L, 4),
                      "best_overlap": round(a["best_overlap"] / L, 4),
                      "needle_recall": (round(a["needle_hits"] / a["needles"], 4)
@@ -985,6 +1001,7 @@ def run_ablation(args, dev) -> dict:
                      "needle_recall": (round(bacc["needle_hits"] / bacc["needles"], 4)
                                        if bacc["needles"] else None)})
     return {"rows": rows,
+            "default_recall_per_layer": depth,
             "workload": {"tokens": n, "layers": L, "h_q": w.h_q, "h_kv": w.h_kv, "d": d, "B": B,
                          "data": args.ablation_data, "dtype": w.dtype,
                          "topic_drift": args.ablation_drift if args.ablation_data == "topics" else None,
@@ -1017,7 +1034,7 @@ def main() -> int:
                     help="instead of the benchmark line, print selection recall on planted "
                          "synthetic data against r, s, density, walk on/off and transition")
     ap.add_argument("--ablation-tokens", type=int, default=16384)
-    ap.add_argument("--ablation-layers", type=int, default=4)
+    ap.add_argument("--ablation-layers", type=int, default=8)
     ap.add_argument("--ablation-needles", type=int, default=16)
     ap.add_argument("--ablation-drift", type=float, default=0.0,
                     help="topic data: share of blocks that change topic at each layer")
