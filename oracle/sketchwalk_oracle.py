@@ -111,8 +111,11 @@ def head_mean(X) -> np.ndarray:
     Under GQA the query average runs over the h_q query heads and the key
     average over the h_kv KV heads (each KV head stands for G query heads, so
     this equals the average over the expanded key heads)."""
-    X = f64(X)
-    return X.sum(axis=0) / X.shape[0]
+    h, n, d = X.shape
+    out = np.empty((n, d), dtype=np.float64)
+    for a in range(0, n, 4096):          # token chunks (each token's sum is independent)
+        out[a:a + 4096] = f64(X[:, a:a + 4096]).sum(axis=0) / h
+    return out
 
 
 def block_means(Xa: np.ndarray, B: int) -> np.ndarray:
@@ -445,7 +448,7 @@ def decode_state_from_prefill(Q, K, B: int, signs, cols, b_max: int) -> DecodeLa
     means, the head-averaged tokens of the last (possibly partial) block, the
     prefill score matrix and its scale."""
     sk = sketch_scores(Q, K, B, signs, cols)
-    n = f64(Q).shape[1]
+    n = Q.shape[1]
     b = sk["qbar"].shape[0]
     d = sk["qbar"].shape[1]
     qbar = np.zeros((b_max, d))
@@ -455,8 +458,8 @@ def decode_state_from_prefill(Q, K, B: int, signs, cols, b_max: int) -> DecodeLa
     A = np.zeros((b_max, b_max))
     A[:b, :b] = sk["A"]
     first = (b - 1) * B                      # first token of the last block
-    qtok = head_mean(f64(Q)[:, first:n])
-    ktok = head_mean(f64(K)[:, first:n])
+    qtok = head_mean(Q[:, first:n])
+    ktok = head_mean(K[:, first:n])
     return DecodeLayerState(qbar, kbar, qtok, ktok, A, sk["c"])
 
 
@@ -508,17 +511,19 @@ def decode_attention(q, Kc, Vc, sel: Sequence[int], p: int, B: int,
                      scale: Optional[float] = None) -> np.ndarray:
     """Alg. 2 step 7: per query head u, softmax over the tokens t <= p of the
     selected blocks of KV head u // G. q [h_q][d], Kc/Vc [h_kv][T][d]."""
-    q, Kc, Vc = f64(q), f64(Kc), f64(Vc)
+    q = f64(q)
     h_q, d = q.shape
     G = h_q // Kc.shape[0]
     sc = (1.0 / math.sqrt(d)) if scale is None else scale
     toks = np.concatenate([np.arange(j * B, min(p + 1, (j + 1) * B)) for j in sorted(sel)])
+    Ks = f64(Kc[:, toks.tolist()])          # the selected tokens only, [h_kv][tokens][d]
+    Vs = f64(Vc[:, toks.tolist()])
     out = np.zeros((h_q, d))
     for u in range(h_q):
         g = u // G
-        logits = (Kc[g, toks] @ q[u]) * sc
+        logits = (Ks[g] @ q[u]) * sc
         e = np.exp(logits - np.max(logits))
-        out[u] = (e @ Vc[g, toks]) / e.sum()
+        out[u] = (e @ Vs[g]) / e.sum()
     return out
 
 
