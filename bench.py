@@ -200,6 +200,35 @@ def cpu_baseline_decode(budget_s: float = 10.0, layers: int = 4, seed: int = 0) 
     }
 
 
+def decode_step_bytes(p: int, n0: int, B: int, h_q: int, h_kv: int, d: int, r: int, pct: int,
+                      esz: int = 2) -> dict:
+    """Algorithmic HBM bytes of one (sequence, layer) decode step for the
+    token at position p of a sequence whose prompt had n0 tokens (density
+    pct, forced first and current blocks), by category:
+      kv      K and V of the selected tokens: tau - 1 whole blocks plus the
+              current block's tokens up to p (the current block is always
+              selected, every other selected block precedes it);
+      qo      the query and the output of every query head;
+      walk    the score-cache entries the walk row reads (fp32): row m holds
+              blocks j <= m, and the columns decode filled (col0..b_cur) hold
+              every row;
+      sketch  the block sketches the score updates read (fp64 Qs and Ks of
+              the earlier blocks);
+      writes  the appended K/V token and the new score row and column."""
+    bc = p // B
+    col0 = n0 // B
+    tau = min(max((bc + 1) * pct // 100 + (1 if (bc + 1) * pct % 100 else 0), 2), bc + 1)
+    toks = (tau - 1) * B + (p - bc * B + 1)
+    walk_entries = (bc + 1) * (bc + 2) // 2 + sum(range(col0, bc + 1))
+    return {
+        "kv": toks * h_kv * d * esz * 2,
+        "qo": 2 * h_q * d * esz,
+        "walk": walk_entries * 4,
+        "sketch": 2 * bc * r * 8,
+        "writes": 2 * h_kv * d * esz + (2 * bc + 1) * 4,
+    }
+
+
 def run_decode(args, dev) -> dict:
     """Decode workload: batch 16, 65536-token prompt per sequence, 32 layers,
     256 single-token steps, every layer walked. Returns the decode block of
@@ -347,6 +376,13 @@ def run_decode(args, dev) -> dict:
     achieved = attn_bytes / (attn_ms * 1e-3) / 1e9
     step_ms = total_ms / n_timed
     sel_ms = step_ms / L - attn_ms
+    # algorithmic bytes of the timed steps (positions n0 .. n0 + n_timed - 1)
+    cats = {}
+    for k in range(n_timed):
+        for key, v in decode_step_bytes(n0 + k, n0, B, w.h_q, w.h_kv, w.d, w.r, w.pct).items():
+            cats[key] = cats.get(key, 0) + v * batch * L
+    step_bytes = sum(cats.values()) / n_timed
+    step_gbs = step_bytes / (step_ms * 1e-3) / 1e9
     return {
         "workload": "decode: batch 16, 65536-token KV cache, 32 q / 8 kv heads, head_dim 128, block 64, "
                     "bf16, 32 layers, 256 steps, density 20%",
@@ -358,6 +394,13 @@ def run_decode(args, dev) -> dict:
         "attention_ms_per_layer": round(attn_ms, 4),
         "rest_ms_per_layer": round(sel_ms, 4),
         "overhead_pct": round(100.0 * max(sel_ms, 0.0) / (step_ms / L), 2),
+        "hbm_step": {
+            "what": "algorithmic bytes of the whole step (selected K/V, q/o, walk-row score-cache "
+                    "reads, block-sketch reads, appends and score writes) over the step time",
+            "bytes_per_step": round(step_bytes), "achieved": round(step_gbs, 1),
+            "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(step_gbs / PEAK_HBM_GBS, 4),
+            "share": {key: round(v / n_timed / step_bytes, 4) for key, v in cats.items()},
+        },
         "roofline": {
             "kernel": "attn_decode_mfma_kernel<128> + attn_merge_kernel",
             "bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",

@@ -110,7 +110,8 @@ int sw_select_max_count(int n_seqs, const int32_t* cu_seqlens /* [host] */, int 
  * range-checked); 1 <= r <= d.
  * Outputs (float64): Qs, Ks [nb][r]; A [nm]; A_scale [n_seqs]; Qbar, Kbar
  * [nb][d] block means (optional, may be NULL).
- * workspace: >= sw_sketch_workspace_bytes(...) bytes, 256-byte aligned.
+ * workspace: >= sw_sketch_workspace_bytes(...) bytes, 256-byte aligned (the
+ * current kernels need none: the query returns 0 and workspace may be NULL).
  */
 int sw_sketch_scores(int dtype, const void* Q, const void* K, int h_q, int h_kv, int d,
                      int n_seqs, const int32_t* cu_seqlens /* [host] */, int B,
@@ -214,14 +215,18 @@ int sw_sparse_attn_prefill(int dtype, const void* Q, const void* K, const void* 
  *   double A_scale[batch]         score scale c (frozen at its prefill value)
  *   int32  col0[batch]            first key block whose column decode fills
  *                                 (= prompt length / B)
- *   int32  cnt[batch][2]          token counts of the open query / key block
- *   double bar[batch][2][d]       running means of the open query / key block
+ *   int32  cnt[batch][2][2]       token counts of the open query / key block,
+ *                                 two copies: the step at position p reads
+ *                                 copy (p + 1) % 2 and writes copy p % 2
+ *   double bar[batch][2][2][d]    running means of the open query / key block,
+ *                                 two copies as for cnt
  *   double qt[batch][r]           sketch of the latest token's query
  *   double Qs[batch][b_max][r]    sketch of every query-block representative
  *   double Ks[batch][b_max][r]    sketch of every key-block representative
  *   float  A[batch][b_max][lda]   block-score cache (fp32), lda = b_max rounded
  *                                 up to a multiple of 4
- * Checkpointing a decode is a byte copy of this buffer (plus the caches).
+ * Checkpointing a decode is a byte copy of this buffer (plus the caches)
+ * taken between calls.
  * pos [batch] int32 (device): 0-based position of the new token of each
  * sequence; b_cur = pos / B is the open block. Sequences whose pos is
  * negative, >= T_max (attention, append) or beyond b_max blocks are skipped:
@@ -325,9 +330,9 @@ int sw_sparse_attn_decode(int dtype, const void* q, const void* Kc, const void* 
  * from that of layer l-1; layer 0 is the first walked layer). Per layer it
  * enqueues the same arithmetic as sw_kv_append + sw_sketch_scores_decode +
  * sw_walk_update_decode_variant + sw_select_topk_blocks_decode +
- * sw_sparse_attn_decode, with the KV append fused into the incremental sketch
- * and the walk row's normalisation fused into the selection (6 kernel
- * launches per layer instead of 8); results are bit-identical to those
+ * sw_sparse_attn_decode, with the KV append and the score updates in one
+ * kernel and the walk row's normalisation fused into the selection (5 kernel
+ * launches per layer instead of 7); results are bit-identical to those
  * calls.
  *
  * Layer-stacked, contiguous buffers (device):

@@ -193,7 +193,7 @@ int sw_sketch_scores(int dtype, const void* Q, const void* K, int h_q, int h_kv,
   if (Qbar && !aligned(Qbar, 8)) return fail(SW_ERR_INVALID_ARG, "Qbar misaligned");
   if (Kbar && !aligned(Kbar, 8)) return fail(SW_ERR_INVALID_ARG, "Kbar misaligned");
   const int64_t need = sw::sketch_workspace_bytes(h_q, h_kv, d, nb);
-  CHECK(check_ptr(workspace, 256, "workspace"));
+  if (need > 0) CHECK(check_ptr(workspace, 256, "workspace"));
   if (workspace_bytes < need)
     return fail(SW_ERR_INVALID_ARG, "workspace_bytes=%lld < required %lld",
                 (long long)workspace_bytes, (long long)need);
@@ -392,7 +392,7 @@ int sw_walk_update_decode_variant(int variant, const void* state, int batch, int
   CHECK(check_ptr(r_out, 8, "r_out"));
   if (r_prev && !aligned(r_prev, 8)) return fail(SW_ERR_INVALID_ARG, "r_prev misaligned");
   if (r_prev == r_out) return fail(SW_ERR_INVALID_ARG, "r_out aliases r_prev");
-  hipError_t e = sw::launch_decode_walk(reinterpret_cast<const char*>(state), batch, d, r, b_max, B,
+  hipError_t e = sw::launch_decode_walk(static_cast<const char*>(state), batch, d, r, b_max, B,
                                         pos, s, variant == SW_WALK_RELU, r_prev, r_out,
                                         reinterpret_cast<hipStream_t>(stream));
   return hip_status(e, "sw_walk_update_decode launch");
@@ -548,11 +548,9 @@ int sw_decode_step(int dtype, int layers, int batch, int h_q, int h_kv, int d, i
                                             h_kv, d, B, pos, signs, cols, r, b_max, stl, st,
                                             vb + l * kv_step, Kl, Vl, T_max);
     if (e == hipSuccess)
-      e = sw::launch_decode_walk(stl, batch, d, r, b_max, B, pos, s, walk_variant == SW_WALK_RELU,
-                                 l == 0 ? nullptr : rl - row_step, rl, st, /*normalize=*/false);
-    if (e == hipSuccess)
-      e = sw::launch_select_decode(rl, batch, b_max, B, pos, k, density_pct, flags, il, cl, kmax,
-                                   st, /*normalize_rows=*/rl);
+      e = sw::launch_decode_walk_select(stl, batch, d, r, b_max, B, pos, s,
+                                        walk_variant == SW_WALK_RELU, l == 0 ? nullptr : rl - row_step,
+                                        rl, k, density_pct, flags, il, cl, kmax, st);
     if (e == hipSuccess)
       e = sw::launch_attn_decode(dtype, qb + l * q_step, Kl, Vl, batch, h_q, h_kv, d, T_max, B, pos,
                                  il, cl, kmax, scale, Ob + l * q_step,

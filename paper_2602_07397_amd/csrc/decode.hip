@@ -3,30 +3,30 @@
 //
 //  decode_init_kernel     state of one sequence from its prompt's prefill sketch
 //  kv_append_kernel       step 1: K_t, V_t into the caches at pos[b]
-//  decode_reps_kernel     steps 2-3 (one workgroup per sequence): running means
-//                         of the open query/key block, SRHT (in-LDS FWHT) of the
-//                         token query and of both open representatives
-//  decode_scores_kernel   step 4 over (sequence, 64-row chunk) workgroups, 4
-//                         lanes per sketch row: (i) new score row (token query
-//                         vs every earlier key block), (ii) new last column
-//                         (every query block vs the open key block)
-//  walk_row_strip_kernel  step 5 on the query row only: r = W[b_q, :] at the
-//                         first walked layer, else r_prev W with W = (A/c)^s
-//                         (or the clipped power) taken while streaming the fp32
-//                         score cache; one workgroup per (sequence, 16-column
-//                         strip), SW_STRIP_RG row groups reduced in LDS in a
-//                         fixed order (16 columns measured 10 % faster than
-//                         32 or 64: the longest strips set the time)
-//  walk_row_norm_kernel   divides the row by its largest magnitude
+//  decode_sketch_kernel   steps 2-4 over (sequence, 64-row chunk) workgroups:
+//                         every workgroup forms the running means of the open
+//                         query/key block and the SRHT of the token query and
+//                         of both open representatives (wavefront-level
+//                         Walsh-Hadamard transforms); chunk 0 stores them (and
+//                         appends K_t, V_t in the one-call step); then each
+//                         workgroup writes its rows' entries of (i) the new
+//                         score row and (ii) the new last column, 4 lanes per
+//                         sketch row
+//  walk_strip_kernel      step 5 on the query row only: r = W[b_q, :] at the
+//                         first walked layer, else r_prev W with W = (A/c)^s (or
+//                         the clipped power) taken while streaming the fp32
+//                         score cache; one workgroup per (sequence, pair of
+//                         32-column strips), the pairs balanced so that every
+//                         workgroup reads about as many rows, 32 row groups
+//                         reduced in LDS in a fixed order
+//  walk_row_norm_kernel   divides the row by its largest magnitude (the
+//                         one-call step does this in select_decode_norm_kernel
+//                         before selecting, step 6)
+#include "select_row.h"
 #include "sw_common.h"
 #include "sw_internal.h"
 
 namespace sw {
-
-// Tuning constants (overridable at build time).
-#ifndef SW_STRIP_RG
-#define SW_STRIP_RG 64        // row groups per walk-row strip workgroup
-#endif
 
 __device__ __forceinline__ double pow_int_d(double x, int s) {
   if (s == 8) {               // the paper's default exponent: three squarings
@@ -70,17 +70,19 @@ __global__ __launch_bounds__(256) void decode_init_kernel(char* __restrict__ sta
   }
   if (m == 0) {
     const int last = n - (b - 1) * B;    // tokens in the last (open) block
-    double* bar = reinterpret_cast<double*>(state + L.bar) + (long long)seq * 2 * d;
+    double* bar = reinterpret_cast<double*>(state + L.bar) + (long long)seq * 4 * d;
     for (int t = threadIdx.x; t < d; t += 256) {
-      bar[t] = Qbar[(long long)(b - 1) * d + t];
-      bar[d + t] = Kbar[(long long)(b - 1) * d + t];
+#pragma unroll
+      for (int c = 0; c < 2; ++c) {      // both position-parity copies
+        bar[(2 * c) * d + t] = Qbar[(long long)(b - 1) * d + t];
+        bar[(2 * c + 1) * d + t] = Kbar[(long long)(b - 1) * d + t];
+      }
     }
     if (threadIdx.x == 0) {
       reinterpret_cast<double*>(state + L.scale)[seq] = A_scale[0];
       reinterpret_cast<int32_t*>(state + L.col0)[seq] = n / B;
-      int32_t* cnt = reinterpret_cast<int32_t*>(state + L.cnt) + seq * 2;
-      cnt[0] = last;
-      cnt[1] = last;
+      int32_t* cnt = reinterpret_cast<int32_t*>(state + L.cnt) + seq * 4;
+      cnt[0] = cnt[1] = cnt[2] = cnt[3] = last;
     }
   }
 }
@@ -106,7 +108,7 @@ __global__ __launch_bounds__(64) void kv_append_kernel(const T* __restrict__ k_n
 }
 
 // ---------------------------------------------------------------------------
-// incremental sketch (one workgroup per sequence)
+// incremental sketch and score updates
 // ---------------------------------------------------------------------------
 
 template <typename T>
@@ -118,30 +120,60 @@ __device__ __forceinline__ float load_f32(const T* p, long long i) {
   }
 }
 
-// APPEND: also writes k_new and v_new into the caches at pos (Alg. 2 step 1;
-// Kc, Vc [batch][h_kv][T_max][d], 16-byte aligned rows).
+constexpr int kScoreChunk = 64;
+
+// Steps 2-4 of the token at pos[b] (one workgroup per (sequence, chunk of 64
+// score rows); every workgroup of a sequence forms the same representatives):
+//   - head sums of the new query and key (thread (group, 16-byte chunk)
+//     adds the heads u = group, group + P, ...; the P groups are then added
+//     per dimension in a fixed order);
+//   - running means of the open query/key block from the previous step's copy
+//     (restarted when pos % B == 0); chunk 0 stores the new copy;
+//   - SRHT of the token query and of both open representatives (three
+//     wavefronts, one transform each); chunk 0 stores them;
+//   - rows j of the chunk: (i) A[b_cur][j] = q~_t . Ks[j] / sqrt(r) for
+//     j < b_cur, (ii) A[j][b_cur] = Qs[j] . Ks[b_cur] / sqrt(r) for j <= b_cur,
+//     four threads per row (coordinates k = 4 i + lane % 4, then two lane
+//     exchanges).
+// APPEND (the one-call step): chunk 0 also writes k_new and v_new into the
+// caches Kc, Vc [batch][h_kv][T_max][d] at pos (Alg. 2 step 1).
 template <typename T, bool APPEND>
-__global__ __launch_bounds__(256) void decode_reps_kernel(const T* __restrict__ q_new,
-                                                          const T* __restrict__ k_new, int h_q,
-                                                          int h_kv, int d, int B,
-                                                          const int32_t* __restrict__ pos,
-                                                          const int8_t* __restrict__ signs,
-                                                          const int32_t* __restrict__ cols, int r,
-                                                          int batch, int b_max,
-                                                          char* __restrict__ state,
-                                                          const T* __restrict__ v_new,
-                                                          T* __restrict__ Kc, T* __restrict__ Vc,
-                                                          int T_max) {
+__global__ __launch_bounds__(256) void decode_sketch_kernel(const T* __restrict__ q_new,
+                                                            const T* __restrict__ k_new, int h_q,
+                                                            int h_kv, int d, int B,
+                                                            const int32_t* __restrict__ pos,
+                                                            const int8_t* __restrict__ signs,
+                                                            const int32_t* __restrict__ cols, int r,
+                                                            int batch, int b_max,
+                                                            char* __restrict__ state,
+                                                            const T* __restrict__ v_new,
+                                                            T* __restrict__ Kc, T* __restrict__ Vc,
+                                                            int T_max) {
   constexpr int V = 16 / (int)sizeof(T);             // elements per 16-byte load
-  __shared__ double xq[256], xk[256], xb[256];
   __shared__ double pq[256 * V], pk[256 * V];
+  __shared__ double xq[256], xb[256], xk[256];
+  __shared__ double sqt[256], sqb[256], skb[256];
   const DecodeLayout L = decode_layout(batch, d, r, b_max);
   const int bi = blockIdx.x;
+  const int chunk = blockIdx.y;
   const int t = threadIdx.x;
+  // the new token's query/key chunks do not depend on the position: their
+  // loads go out first (clamped head indices: no condition; extra ones unused)
+  const int dpc = d / V;                           // chunks per head row
+  const int P = 256 / dpc;                         // head groups
+  const int ch = t % dpc, grp = t / dpc;
+  constexpr int kChunks = 4;                       // head chunks loaded up front
+  uint4 rq[kChunks], rk[kChunks];
+#pragma unroll
+  for (int i = 0; i < kChunks; ++i) {
+    const int u = min(grp + i * P, h_q - 1), g = min(grp + i * P, h_kv - 1);
+    rq[i] = *reinterpret_cast<const uint4*>(q_new + ((long long)bi * h_q + u) * d + ch * V);
+    rk[i] = *reinterpret_cast<const uint4*>(k_new + ((long long)bi * h_kv + g) * d + ch * V);
+  }
   const int p = pos[bi];
   const int bc = p / B;                  // open key block == query block
   if constexpr (APPEND) {
-    if (p >= 0 && p < T_max) {
+    if (chunk == 0 && p >= 0 && p < T_max) {
       const int cpr = d / V;
       for (int c = t; c < h_kv * cpr; c += 256) {
         const int g = c / cpr, o = (c % cpr) * V;
@@ -153,121 +185,131 @@ __global__ __launch_bounds__(256) void decode_reps_kernel(const T* __restrict__ 
     }
   }
   if (p < 0 || bc >= b_max) return;
-  double* bar = reinterpret_cast<double*>(state + L.bar) + (long long)bi * 2 * d;
-  int32_t* cnt = reinterpret_cast<int32_t*>(state + L.cnt) + bi * 2;
+  const int r0 = chunk * kScoreChunk;
+  if (r0 > bc) return;
+  const bool store = chunk == 0;
   double* Qs = reinterpret_cast<double*>(state + L.qs) + (long long)bi * b_max * r;
   double* Ks = reinterpret_cast<double*>(state + L.ks) + (long long)bi * b_max * r;
-  double* qt = reinterpret_cast<double*>(state + L.qt) + (long long)bi * r;
-  // head sums: thread (group, chunk) adds the 16-byte chunk `chunk` (V dims)
-  // of the heads u = group, group + P, ...; then the P groups are added per dim
-  const int dpc = d / V;                           // chunks per head row
-  const int P = 256 / dpc;                         // head groups
-  const int ch = t % dpc, grp = t / dpc;
+  const int rd = (p + 1) & 1, wr = p & 1;          // previous / new copy of the open means
+  const int32_t* cnt_rd = reinterpret_cast<const int32_t*>(state + L.cnt) + (bi * 2 + rd) * 2;
+  int32_t* cnt_wr = reinterpret_cast<int32_t*>(state + L.cnt) + (bi * 2 + wr) * 2;
+  const double* bar_rd = reinterpret_cast<const double*>(state + L.bar) + (long long)(bi * 2 + rd) * 2 * d;
+  double* bar_wr = reinterpret_cast<double*>(state + L.bar) + (long long)(bi * 2 + wr) * 2 * d;
+
+  // Then, in the order the values are needed (vector loads complete in
+  // order): the previous open means and counts, the transform's signs and
+  // columns, and last this thread's score row j of the earlier blocks'
+  // sketches (coordinates k = 4 i + q4), which stay in flight while the
+  // representatives are formed.
+  const int td = min(t, d - 1), tr = min(t, r - 1);   // clamped: no load behind a branch
+  const double bq_old = bar_rd[td], bk_old = bar_rd[d + td];
+  const int8_t sgn = signs[td];
+  const int colv = cols[tr] & (d - 1);
+  const int qc = cnt_rd[0], kc = cnt_rd[1];
+  const int q4 = t & 3;
+  const int j = r0 + (t >> 2);
+  constexpr int kPre = 16;
+  double pre_q[kPre], pre_k[kPre];
+#pragma unroll
+  for (int i = 0; i < kPre; ++i) {
+    const int k = q4 + 4 * i;
+    // clamped (the load carries no condition); rows j >= b_cur are not used
+    const int jj = min(j, max(bc - 1, 0)), kk = min(k, r - 1);
+    pre_q[i] = Qs[(long long)jj * r + kk];
+    pre_k[i] = Ks[(long long)jj * r + kk];
+  }
+
   double sq[V], sk[V];
 #pragma unroll
   for (int e = 0; e < V; ++e) sq[e] = sk[e] = 0.0;
-  auto add_chunk = [&](const T* src, double (&acc)[V]) {
-    const uint4 raw = *reinterpret_cast<const uint4*>(src);
+  auto add_raw = [&](const uint4& raw, double (&acc)[V]) {
     const T* v = reinterpret_cast<const T*>(&raw);
 #pragma unroll
     for (int e = 0; e < V; ++e) acc[e] += (double)load_f32(v, e);
   };
-#pragma unroll 4
-  for (int u = grp; u < h_q; u += P) add_chunk(q_new + ((long long)bi * h_q + u) * d + ch * V, sq);
-#pragma unroll 4
-  for (int g = grp; g < h_kv; g += P) add_chunk(k_new + ((long long)bi * h_kv + g) * d + ch * V, sk);
+#pragma unroll
+  for (int i = 0; i < kChunks; ++i) {
+    if (grp + i * P < h_q) add_raw(rq[i], sq);
+    if (grp + i * P < h_kv) add_raw(rk[i], sk);
+  }
+  for (int u = grp + kChunks * P; u < h_q; u += P)
+    add_raw(*reinterpret_cast<const uint4*>(q_new + ((long long)bi * h_q + u) * d + ch * V), sq);
+  for (int g = grp + kChunks * P; g < h_kv; g += P)
+    add_raw(*reinterpret_cast<const uint4*>(k_new + ((long long)bi * h_kv + g) * d + ch * V), sk);
 #pragma unroll
   for (int e = 0; e < V; ++e) {
     pq[grp * d + ch * V + e] = sq[e];
     pk[grp * d + ch * V + e] = sk[e];
   }
   const bool fresh = (p % B) == 0;
-  const int qc = cnt[0], kc = cnt[1];
   __syncthreads();
-  double qa = 0.0, ka = 0.0, qbn = 0.0, kbn = 0.0;
   if (t < d) {
+    double qa = 0.0, ka = 0.0;
     for (int x = 0; x < P; ++x) {
       qa += pq[x * d + t];
       ka += pk[x * d + t];
     }
     qa /= (double)h_q;
     ka /= (double)h_kv;
-    qbn = fresh ? qa : ((double)qc * bar[t] + qa) / (double)(qc + 1);
-    kbn = fresh ? ka : ((double)kc * bar[d + t] + ka) / (double)(kc + 1);
-  }
-  __syncthreads();                       // every read of the old state is done
-  if (t < d) {
-    bar[t] = qbn;
-    bar[d + t] = kbn;
-    const double sg = (double)signs[t];
+    const double qbn = fresh ? qa : ((double)qc * bq_old + qa) / (double)(qc + 1);
+    const double kbn = fresh ? ka : ((double)kc * bk_old + ka) / (double)(kc + 1);
+    if (store) {
+      bar_wr[t] = qbn;
+      bar_wr[d + t] = kbn;
+    }
+    const double sg = (double)sgn;
     xq[t] = qa * sg;
     xb[t] = qbn * sg;
     xk[t] = kbn * sg;
   }
-  if (t == 0) {
-    cnt[0] = fresh ? 1 : qc + 1;
-    cnt[1] = fresh ? 1 : kc + 1;
+  if (store && t == 0) {
+    cnt_wr[0] = fresh ? 1 : qc + 1;
+    cnt_wr[1] = fresh ? 1 : kc + 1;
   }
   __syncthreads();
-  for (int len = 1; len < d; len <<= 1) {
-    if (t < d / 2) {
-      const int a = (t / len) * 2 * len + (t % len);
-      double u, v;
-      u = xq[a]; v = xq[a + len]; xq[a] = u + v; xq[a + len] = u - v;
-      u = xb[a]; v = xb[a + len]; xb[a] = u + v; xb[a + len] = u - v;
-      u = xk[a]; v = xk[a + len]; xk[a] = u + v; xk[a + len] = u - v;
-    }
-    __syncthreads();
-  }
+  const int wave = t >> 6;
+  if (wave == 0) wave_fwht(xq, d);
+  else if (wave == 1) wave_fwht(xb, d);
+  else if (wave == 2) wave_fwht(xk, d);
+  __syncthreads();
   const double rs = 1.0 / sqrt((double)r);
   if (t < r) {
-    const int c = cols[t] & (d - 1);
-    qt[t] = xq[c] * rs;
-    Qs[(long long)bc * r + t] = xb[c] * rs;
-    Ks[(long long)bc * r + t] = xk[c] * rs;
+    sqt[t] = xq[colv] * rs;
+    sqb[t] = xb[colv] * rs;
+    skb[t] = xk[colv] * rs;
+    if (store) {
+      reinterpret_cast<double*>(state + L.qt)[(long long)bi * r + t] = sqt[t];
+      Qs[(long long)bc * r + t] = sqb[t];
+      Ks[(long long)bc * r + t] = skb[t];
+    }
   }
-}
-
-constexpr int kScoreChunk = 64;
-
-// Rows [64c, 64c+64): row entries A[bc][j] (j < bc) and column entries
-// A[m][bc] (m <= bc), four threads per row.
-__global__ __launch_bounds__(256) void decode_scores_kernel(const int32_t* __restrict__ pos, int r,
-                                                            int B, int batch, int d, int b_max,
-                                                            char* __restrict__ state) {
-  const DecodeLayout L = decode_layout(batch, d, r, b_max);
-  const int bi = blockIdx.x;
-  const int c = blockIdx.y;
-  const int p = pos[bi];
-  const int bc = p / B;
-  if (p < 0 || bc >= b_max) return;
-  const int r0 = c * kScoreChunk;
-  if (r0 > bc) return;
-  const double* Qs = reinterpret_cast<const double*>(state + L.qs) + (long long)bi * b_max * r;
-  const double* Ks = reinterpret_cast<const double*>(state + L.ks) + (long long)bi * b_max * r;
-  const double* qt = reinterpret_cast<const double*>(state + L.qt) + (long long)bi * r;
-  float* A = reinterpret_cast<float*>(state + L.a) + (long long)bi * b_max * L.lda;
-  const double rs = 1.0 / sqrt((double)r);
-  // four threads per row j (kScoreChunk rows per workgroup); thread q4 takes
-  // the sketch coordinates k = 4 i + q4, all loads independent
-  const int t = threadIdx.x;
-  const int q4 = t & 3;
-  const int j = r0 + (t >> 2);
+  __syncthreads();
+  // Qs[b_cur] and Ks[b_cur] are taken from LDS: chunk 0 may be storing them
   double accr = 0.0, accc = 0.0;
-  if (j <= bc) {
+  if (j < bc) {
+#pragma unroll
+    for (int i = 0; i < kPre; ++i) {
+      const int k = q4 + 4 * i;
+      if (k < r) {
+        accc += pre_q[i] * skb[k];
+        accr += sqt[k] * pre_k[i];
+      }
+    }
     const double* qsj = Qs + (long long)j * r;
     const double* ksj = Ks + (long long)j * r;
-    const double* ksb = Ks + (long long)bc * r;
-#pragma unroll 16
-    for (int k = q4; k < r; k += 4) {
-      accc += qsj[k] * ksb[k];
-      accr += qt[k] * ksj[k];
+    for (int k = q4 + 4 * kPre; k < r; k += 4) {
+      accc += qsj[k] * skb[k];
+      accr += sqt[k] * ksj[k];
     }
+  } else if (j == bc) {
+#pragma unroll 16
+    for (int k = q4; k < r; k += 4) accc += sqb[k] * skb[k];
   }
   accr += __shfl_xor(accr, 1);
   accc += __shfl_xor(accc, 1);
   accr += __shfl_xor(accr, 2);
   accc += __shfl_xor(accc, 2);
+  float* A = reinterpret_cast<float*>(state + L.a) + (long long)bi * b_max * L.lda;
   if (q4 == 0 && j <= bc) {
     if (j < bc) A[(long long)bc * L.lda + j] = (float)(accr * rs);
     A[(long long)j * L.lda + bc] = (float)(accc * rs);
@@ -278,95 +320,177 @@ __global__ __launch_bounds__(256) void decode_scores_kernel(const int32_t* __res
 // walk row
 // ---------------------------------------------------------------------------
 
-constexpr int kStrip = 16;               // columns per workgroup (4 lanes x 4)
-constexpr int kRowGroups = SW_STRIP_RG;  // row groups per workgroup
-constexpr int kStripThreads = (kStrip / 4) * kRowGroups;
+constexpr int kStripCols = 32;           // columns per strip: one 128-byte piece of a row
+constexpr int kStripQuads = kStripCols / 4;
+#ifndef SW_STRIP_GROUPS
+#define SW_STRIP_GROUPS 32               // row groups per workgroup
+#endif
+constexpr int kStripGroups = SW_STRIP_GROUPS;
+constexpr int kStripThreads = kStripQuads * kStripGroups;
+#ifndef SW_STRIP_ROWS
+#define SW_STRIP_ROWS 10                 // rows each thread loads before adding
+#endif
+constexpr int kStripBufWord3 = 0x00020000;   // raw buffer descriptor word 3 (gfx9 family)
 
-// S8: s = 8, the paper's exponent (three squarings, no loop). RELU: negative
-// scores are clipped to zero before the power.
 template <bool S8, bool RELU>
-__global__ __launch_bounds__(kStripThreads) void walk_row_strip_kernel(const char* __restrict__ state,
-                                                             int batch, int d, int r, int b_max,
-                                                             int B, const int32_t* __restrict__ pos,
-                                                             int s_exp,
-                                                             const double* __restrict__ r_prev,
-                                                             double* __restrict__ r_out) {
-  __shared__ double red[kRowGroups][kStrip];
+__device__ __forceinline__ double walk_weight(float a, double inv_c, int s_exp) {
+  double x = (double)a * inv_c;
+  if constexpr (RELU) x = fmax(x, 0.0);
+  if constexpr (S8) {
+    const double x2 = x * x, x4 = x2 * x2;
+    return x4 * x4;
+  } else {
+    return pow_int_d(x, s_exp);
+  }
+}
+
+// One workgroup per (sequence, strip pair): strips k and S-1-k of 32 columns
+// (S = ceil(lda / 32)), so that every workgroup reads about b_cur rows in all.
+// Strip x needs the rows m >= 32 x (the causal part), or every row when decode
+// filled one of its columns (col0 <= j <= b_cur). The row groups are shared
+// between the two strips in proportion to their row counts; thread (row
+// group g, column quad q) takes every n-th row of its strip (n = the strip's
+// group count), 16-byte loads of 4 columns, a row of a strip being one
+// 128-byte piece. r_out[j] = sum over those rows m (per group ascending, then
+// over the strip's groups in blocks of 8, then over the blocks, each in
+// order) of r_prev[m] W[m][j]. Entries the score cache
+// holds as zero (above the diagonal outside the decode-filled columns, past
+// b_cur) give zero terms, so no per-element mask is needed; quads that are
+// wholly zero are not loaded. At the first walked layer (r_prev NULL) the
+// row of W itself, r_out[j] = W[b_cur][j]. Entries past b_cur are 0.
+template <bool S8, bool RELU>
+__global__ __launch_bounds__(kStripThreads) void walk_strip_kernel(const char* __restrict__ state,
+                                                                   int batch, int d, int r,
+                                                                   int b_max, int B,
+                                                                   const int32_t* __restrict__ pos,
+                                                                   int s_exp,
+                                                                   const double* __restrict__ r_prev,
+                                                                   double* __restrict__ r_out) {
+  // the walk row of the previous layer during the row loop, then the row
+  // groups' sums (both fit: b_max <= 4096 <= kStripGroups * kStripCols)
+  __shared__ double smem[kStripGroups * kStripCols > SW_MAX_BLOCKS ? kStripGroups * kStripCols
+                                                                   : SW_MAX_BLOCKS];
   const DecodeLayout L = decode_layout(batch, d, r, b_max);
+  const int lda = L.lda;
   const int bi = blockIdx.x;
-  const int j0 = blockIdx.y * kStrip;
+  const int k = blockIdx.y;
+  const int t = threadIdx.x;
+  // the loads that do not need the position go out with it: the scale, the
+  // first decode-filled column and the whole previous walk row (clamped
+  // indices, no condition), which is then staged in LDS
   const int p = pos[bi];
+  const double c0 = reinterpret_cast<const double*>(state + L.scale)[bi];
+  const int col0 = reinterpret_cast<const int32_t*>(state + L.col0)[bi];
+  constexpr int kStage = (SW_MAX_BLOCKS + kStripThreads - 1) / kStripThreads;
+  if (r_prev != nullptr) {
+    double rs[kStage];
+#pragma unroll
+    for (int i = 0; i < kStage; ++i)
+      rs[i] = r_prev[(long long)bi * b_max + min(t + i * kStripThreads, b_max - 1)];
+#pragma unroll
+    for (int i = 0; i < kStage; ++i)
+      if (t + i * kStripThreads < b_max) smem[t + i * kStripThreads] = rs[i];
+  }
   const int bc = p / B;
   if (p < 0 || bc >= b_max) return;
-  if (j0 > bc) return;
-  const double c0 = reinterpret_cast<const double*>(state + L.scale)[bi];
+  const int S = (lda + kStripCols - 1) / kStripCols;
+  const int sa = k, sb = S - 1 - k;                 // sb == sa: a single strip
   const double inv_c = 1.0 / (c0 > 0.0 ? c0 : 1.0);
-  const int col0 = reinterpret_cast<const int32_t*>(state + L.col0)[bi];
-  const float* A = reinterpret_cast<const float*>(state + L.a) + (long long)bi * b_max * L.lda;
-  auto pw = [&](double x) {
-    if constexpr (RELU) x = fmax(x, 0.0);
-    if constexpr (S8) {
-      const double x2 = x * x, x4 = x2 * x2;
-      return x4 * x4;
-    } else {
-      return pow_int_d(x, s_exp);
-    }
+  const float* A = reinterpret_cast<const float*>(state + L.a) + (long long)bi * b_max * lda;
+  const int q = t % kStripQuads, g = t / kStripQuads;
+  auto first_row = [&](int x) {
+    const int j0 = x * kStripCols;
+    return (j0 + kStripCols - 1 >= col0) ? 0 : j0;
   };
-  const int t = threadIdx.x;
-  const int cq = t % (kStrip / 4), rg = t / (kStrip / 4);
-  const int j = j0 + cq * 4;                       // first of this thread's 4 columns
-  const bool jok = j < L.lda;                      // lda % 4 == 0: j..j+3 inside the row
+  const int ma = first_row(sa), mb = first_row(sb);
+  const int na = (sa * kStripCols <= bc) ? bc - ma + 1 : 0;
+  const int nbr = (sb != sa && sb * kStripCols <= bc) ? bc - mb + 1 : 0;
+  const int total = na + nbr;
+  // row groups of strip a: about kStripGroups * na / total (each strip with
+  // rows gets at least one)
+  int ga = (nbr == 0) ? kStripGroups
+                      : (na == 0 ? 0 : (int)(((long long)kStripGroups * na + total / 2) / total));
+  if (na > 0 && nbr > 0) ga = min(max(ga, 1), kStripGroups - 1);
+  const bool in_a = g < ga;
+  const int x = in_a ? sa : sb;
+  const int gi = in_a ? g : g - ga;                 // group index within the strip
+  const int ng = in_a ? ga : kStripGroups - ga;     // groups of the strip
+  const int m0 = in_a ? ma : mb;
+  const int nrows = in_a ? na : nbr;
+  const int j = x * kStripCols + 4 * q;             // this thread's 4 columns
+  const bool okj = j <= bc;                          // the quad holds a block
   double acc[4] = {0.0, 0.0, 0.0, 0.0};
-  if (!jok) {
-    // columns past the padded row: nothing to accumulate
-  } else if (r_prev == nullptr) {
-    // first walked layer: the query row of W itself
-    if (rg == 0) {
-      const float4 a = *reinterpret_cast<const float4*>(A + (long long)bc * L.lda + j);
+  if (r_prev == nullptr) {
+    if (gi == 0 && nrows > 0 && okj) {
+      const float4 a = *reinterpret_cast<const float4*>(A + (long long)bc * lda + j);
       const float av[4] = {a.x, a.y, a.z, a.w};
 #pragma unroll
-      for (int e = 0; e < 4; ++e) acc[e] = pw((double)av[e] * inv_c);
+      for (int e = 0; e < 4; ++e) acc[e] = walk_weight<S8, RELU>(av[e], inv_c, s_exp);
     }
   } else {
-    const double* rp = r_prev + (long long)bi * b_max;
-    // rows that can be non-zero in these columns: m >= column (causal) or any
-    // row for the columns decode filled (>= col0)
-    const int mstart = (j0 + kStrip - 1 >= col0) ? 0 : j0;
-    int m = mstart + rg;
-    for (; m + 7 * kRowGroups <= bc; m += 8 * kRowGroups) {
-      float4 a[8];
-      double w[8];
+    __syncthreads();                     // the staged row is visible
+    // the sequence's score cache as a buffer: 32-bit offsets, and a load
+    // whose quad holds nothing is sent past the end (it reads zeros)
+    const int bytes = b_max * lda * 4;
+    const __amdgpu_buffer_rsrc_t ra =
+        __builtin_amdgcn_make_buffer_rsrc((void*)A, (short)0, bytes, kStripBufWord3);
+    constexpr int NR = S8 ? SW_STRIP_ROWS : SW_STRIP_ROWS / 2;   // the general power needs more registers
+    for (int i0 = gi; i0 < nrows; i0 += NR * ng) {
+      // every load of the pass is issued before any is used
+      uint4 a[NR];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        a[u] = *reinterpret_cast<const float4*>(A + (long long)(m + u * kRowGroups) * L.lda + j);
-        w[u] = rp[m + u * kRowGroups];
+      for (int v = 0; v < NR; ++v) {
+        const int i = i0 + v * ng;
+        const int m = m0 + min(i, nrows - 1);
+        const bool ok = i < nrows && okj && (j <= m || j + 3 >= col0);
+        const int off = ok ? (m * lda + j) * 4 : bytes;
+        a[v] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(ra, off, 0, 0));
       }
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int mm = m + u * kRowGroups;
-        const float av[4] = {a[u].x, a[u].y, a[u].z, a[u].w};
+      for (int v = 0; v < NR; ++v) {
+        const int i = i0 + v * ng;
+        const double rv = smem[m0 + min(i, nrows - 1)];
+        const float av[4] = {__uint_as_float(a[v].x), __uint_as_float(a[v].y),
+                             __uint_as_float(a[v].z), __uint_as_float(a[v].w)};
 #pragma unroll
-        for (int e = 0; e < 4; ++e)
-          acc[e] += (j + e <= mm || j + e >= col0) ? w[u] * pw((double)av[e] * inv_c) : 0.0;
+        for (int e = 0; e < 4; ++e) acc[e] += rv * walk_weight<S8, RELU>(av[e], inv_c, s_exp);
       }
-    }
-    for (; m <= bc; m += kRowGroups) {
-      const float4 a = *reinterpret_cast<const float4*>(A + (long long)m * L.lda + j);
-      const double wv = rp[m];
-      const float av[4] = {a.x, a.y, a.z, a.w};
-#pragma unroll
-      for (int e = 0; e < 4; ++e)
-        acc[e] += (j + e <= m || j + e >= col0) ? wv * pw((double)av[e] * inv_c) : 0.0;
     }
   }
+  __syncthreads();                       // the previous row is no longer read
+  double* red = smem;                    // [kStripGroups][kStripCols]
 #pragma unroll
-  for (int e = 0; e < 4; ++e) red[rg][cq * 4 + e] = acc[e];
+  for (int e = 0; e < 4; ++e) red[g * kStripCols + 4 * q + e] = acc[e];
   __syncthreads();
-  if (t < kStrip) {
+  // fixed-order reduction over a strip's groups: sums of 8 consecutive groups
+  // (one per thread: strip, block of 8 groups, column), then of the blocks
+  constexpr int kBlk = kStripGroups / 8;
+  __shared__ double red2[2][kBlk][kStripCols];
+  {
+    const int which = t / (kBlk * kStripCols), bk = (t / kStripCols) % kBlk, c = t % kStripCols;
+    const int g0 = which ? ga : 0, g1 = which ? kStripGroups : ga;
+    double vals[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) vals[u] = red[(bk * 8 + u) * kStripCols + c];
     double v = 0.0;
-    for (int g = 0; g < kRowGroups; ++g) v += red[g][t];
-    const int jj = j0 + t;
-    if (jj < b_max) r_out[(long long)bi * b_max + jj] = (jj <= bc) ? v : 0.0;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v += (bk * 8 + u >= g0 && bk * 8 + u < g1) ? vals[u] : 0.0;
+    red2[which][bk][c] = v;
+  }
+  __syncthreads();
+  if (t < 2 * kStripCols) {
+    const int which = t / kStripCols, c = t % kStripCols;
+    if (which == 0 || sb != sa) {
+      const int xs = which ? sb : sa;
+      double vals[kBlk];
+#pragma unroll
+      for (int u = 0; u < kBlk; ++u) vals[u] = red2[which][u][c];
+      double v = 0.0;
+#pragma unroll
+      for (int u = 0; u < kBlk; ++u) v += vals[u];
+      const int jj = xs * kStripCols + c;
+      if (jj < b_max) r_out[(long long)bi * b_max + jj] = (jj <= bc) ? v : 0.0;
+    }
   }
 }
 
@@ -387,6 +511,51 @@ __global__ __launch_bounds__(256) void walk_row_norm_kernel(int b_max, int B,
   mx = fmax(fmax(tmp[0], tmp[1]), fmax(tmp[2], tmp[3]));
   const double inv = mx > 0.0 ? 1.0 / mx : 1.0;
   for (int j = threadIdx.x; j < b_max; j += 256) out[j] = (j <= bc) ? out[j] * inv : 0.0;
+}
+
+// The one-call step: the walk row of each sequence divided in place by its
+// largest magnitude over blocks 0..b_cur (entries past b_cur zeroed), then its
+// selection (Alg. 2 step 6, forced set {0, b_cur}) from the rescaled values
+// the threads still hold in registers.
+__global__ __launch_bounds__(256) void select_decode_norm_kernel(double* __restrict__ rows,
+                                                                 int b_max, int B,
+                                                                 const int32_t* __restrict__ pos,
+                                                                 int k, int pct, uint32_t flags,
+                                                                 int32_t* __restrict__ idx,
+                                                                 int32_t* __restrict__ cnt,
+                                                                 int kmax) {
+  __shared__ double tmp[4];
+  const int bi = blockIdx.x;
+  const int p = pos[bi];
+  const int bc = p / B;
+  if (p < 0 || bc >= b_max) return;
+  double* row = rows + (long long)bi * b_max;
+  const int avail = bc + 1;
+  const int E = (avail + 255) / 256;
+  const int t = threadIdx.x;
+  double v[kMaxPerThread];
+  load_row_vals(row, avail, v);
+  double mx = 0.0;
+#pragma unroll
+  for (int e = 0; e < kMaxPerThread; ++e)
+    if (e < E && t * E + e < avail) mx = fmax(mx, fabs(v[e]));
+  for (int off = 32; off > 0; off >>= 1) mx = fmax(mx, __shfl_xor(mx, off));
+  if ((t & 63) == 0) tmp[t >> 6] = mx;
+  __syncthreads();
+  mx = fmax(fmax(tmp[0], tmp[1]), fmax(tmp[2], tmp[3]));
+  const double inv = mx > 0.0 ? 1.0 / mx : 1.0;
+#pragma unroll
+  for (int e = 0; e < kMaxPerThread; ++e) {
+    const int j = t * E + e;
+    if (e < E && j < avail) {
+      v[e] = v[e] * inv;
+      row[j] = v[e];
+    }
+  }
+  for (int j = avail + t; j < b_max; j += 256) row[j] = 0.0;
+  const int first = (flags & SW_FORCE_FIRST) ? 0 : -1;
+  const int last = (flags & SW_FORCE_LAST) ? bc : -1;
+  select_row_vals(v, avail, first, last, k, pct, idx + (long long)bi * kmax, cnt + bi, kmax);
 }
 
 // ---------------------------------------------------------------------------
@@ -421,20 +590,37 @@ hipError_t launch_kv_append(int dtype, const void* k_new, const void* v_new, voi
 namespace {
 
 template <typename T>
-void launch_reps(const void* q_new, const void* k_new, int batch, int h_q, int h_kv, int d, int B,
-                 const int32_t* pos, const int8_t* signs, const int32_t* cols, int r, int b_max,
-                 char* state, const void* v_new, void* Kc, void* Vc, int T_max, hipStream_t st) {
+void launch_sketch_t(const void* q_new, const void* k_new, int batch, int h_q, int h_kv, int d,
+                     int B, const int32_t* pos, const int8_t* signs, const int32_t* cols, int r,
+                     int b_max, char* state, const void* v_new, void* Kc, void* Vc, int T_max,
+                     hipStream_t st) {
   const T* q = reinterpret_cast<const T*>(q_new);
   const T* k = reinterpret_cast<const T*>(k_new);
   const T* v = reinterpret_cast<const T*>(v_new);
+  const dim3 grid((unsigned)batch, (unsigned)((b_max + kScoreChunk - 1) / kScoreChunk));
   if (Kc != nullptr)
-    hipLaunchKernelGGL((decode_reps_kernel<T, true>), dim3((unsigned)batch), dim3(256), 0, st, q, k,
-                       h_q, h_kv, d, B, pos, signs, cols, r, batch, b_max, state, v,
-                       reinterpret_cast<T*>(Kc), reinterpret_cast<T*>(Vc), T_max);
+    hipLaunchKernelGGL((decode_sketch_kernel<T, true>), grid, dim3(256), 0, st, q, k, h_q, h_kv, d,
+                       B, pos, signs, cols, r, batch, b_max, state, v, reinterpret_cast<T*>(Kc),
+                       reinterpret_cast<T*>(Vc), T_max);
   else
-    hipLaunchKernelGGL((decode_reps_kernel<T, false>), dim3((unsigned)batch), dim3(256), 0, st, q, k,
-                       h_q, h_kv, d, B, pos, signs, cols, r, batch, b_max, state, v,
-                       static_cast<T*>(nullptr), static_cast<T*>(nullptr), T_max);
+    hipLaunchKernelGGL((decode_sketch_kernel<T, false>), grid, dim3(256), 0, st, q, k, h_q, h_kv, d,
+                       B, pos, signs, cols, r, batch, b_max, state, v, static_cast<T*>(nullptr),
+                       static_cast<T*>(nullptr), T_max);
+}
+
+void launch_strips(const char* state, int batch, int d, int r, int b_max, int B, const int32_t* pos,
+                   int s_exp, bool relu, const double* r_prev, double* r_out, hipStream_t st) {
+  const int lda = (b_max + 3) & ~3;
+  const int S = (lda + kStripCols - 1) / kStripCols;
+  const dim3 grid((unsigned)batch, (unsigned)((S + 1) / 2)), blk(kStripThreads);
+#define SW_STRIP_LAUNCH(S8, RELU)                                                                \
+  hipLaunchKernelGGL((walk_strip_kernel<S8, RELU>), grid, blk, 0, st, state, batch, d, r, b_max, \
+                     B, pos, s_exp, r_prev, r_out)
+  if (s_exp == 8 && !relu) SW_STRIP_LAUNCH(true, false);
+  else if (s_exp == 8) SW_STRIP_LAUNCH(true, true);
+  else if (!relu) SW_STRIP_LAUNCH(false, false);
+  else SW_STRIP_LAUNCH(false, true);
+#undef SW_STRIP_LAUNCH
 }
 
 }  // namespace
@@ -444,37 +630,31 @@ hipError_t launch_decode_sketch(int dtype, const void* q_new, const void* k_new,
                                 const int32_t* cols, int r, int b_max, char* state,
                                 hipStream_t st, const void* v_new, void* Kc, void* Vc, int T_max) {
   if (dtype == SW_BF16)
-    launch_reps<uint16_t>(q_new, k_new, batch, h_q, h_kv, d, B, pos, signs, cols, r, b_max, state,
-                          v_new, Kc, Vc, T_max, st);
+    launch_sketch_t<uint16_t>(q_new, k_new, batch, h_q, h_kv, d, B, pos, signs, cols, r, b_max,
+                              state, v_new, Kc, Vc, T_max, st);
   else
-    launch_reps<float>(q_new, k_new, batch, h_q, h_kv, d, B, pos, signs, cols, r, b_max, state,
-                       v_new, Kc, Vc, T_max, st);
-  const int nch = (b_max + kScoreChunk - 1) / kScoreChunk;
-  hipLaunchKernelGGL(decode_scores_kernel, dim3((unsigned)batch, (unsigned)nch), dim3(256), 0, st,
-                     pos, r, B, batch, d, b_max, state);
+    launch_sketch_t<float>(q_new, k_new, batch, h_q, h_kv, d, B, pos, signs, cols, r, b_max, state,
+                           v_new, Kc, Vc, T_max, st);
   return hipGetLastError();
 }
 
 hipError_t launch_decode_walk(const char* state, int batch, int d, int r, int b_max, int B,
                               const int32_t* pos, int s_exp, bool relu, const double* r_prev,
-                              double* r_out, hipStream_t st, bool normalize) {
-  const int nstrip = (b_max + kStrip - 1) / kStrip;
-  const dim3 grid((unsigned)batch, (unsigned)nstrip), blk(kStripThreads);
-  if (s_exp == 8 && !relu)
-    hipLaunchKernelGGL((walk_row_strip_kernel<true, false>), grid, blk, 0, st, state, batch, d, r,
-                       b_max, B, pos, s_exp, r_prev, r_out);
-  else if (s_exp == 8)
-    hipLaunchKernelGGL((walk_row_strip_kernel<true, true>), grid, blk, 0, st, state, batch, d, r,
-                       b_max, B, pos, s_exp, r_prev, r_out);
-  else if (!relu)
-    hipLaunchKernelGGL((walk_row_strip_kernel<false, false>), grid, blk, 0, st, state, batch, d, r,
-                       b_max, B, pos, s_exp, r_prev, r_out);
-  else
-    hipLaunchKernelGGL((walk_row_strip_kernel<false, true>), grid, blk, 0, st, state, batch, d, r,
-                       b_max, B, pos, s_exp, r_prev, r_out);
-  if (normalize)
-    hipLaunchKernelGGL(walk_row_norm_kernel, dim3((unsigned)batch), dim3(256), 0, st, b_max, B, pos,
-                       r_out);
+                              double* r_out, hipStream_t st) {
+  launch_strips(state, batch, d, r, b_max, B, pos, s_exp, relu, r_prev, r_out, st);
+  hipLaunchKernelGGL(walk_row_norm_kernel, dim3((unsigned)batch), dim3(256), 0, st, b_max, B, pos,
+                     r_out);
+  return hipGetLastError();
+}
+
+hipError_t launch_decode_walk_select(const char* state, int batch, int d, int r, int b_max, int B,
+                                     const int32_t* pos, int s_exp, bool relu,
+                                     const double* r_prev, double* rows, int k, int pct,
+                                     uint32_t flags, int32_t* idx, int32_t* cnt, int kmax,
+                                     hipStream_t st) {
+  launch_strips(state, batch, d, r, b_max, B, pos, s_exp, relu, r_prev, rows, st);
+  hipLaunchKernelGGL(select_decode_norm_kernel, dim3((unsigned)batch), dim3(256), 0, st, rows,
+                     b_max, B, pos, k, pct, flags, idx, cnt, kmax);
   return hipGetLastError();
 }
 

@@ -1,0 +1,150 @@
+// Top-tau selection of one row by one 256-thread workgroup (paper Alg. 1
+// step 7 / Alg. 2 step 6; forced first and last blocks per Sec. 4.1).
+//
+// Thread t owns the contiguous key-block range [t*E, t*E + E), E =
+// ceil(avail / 256), so block-wide scans run in index order. The
+// (tau - |F|)-th largest walk value among the non-forced blocks is found by
+// an 8-pass, 8-bit MSB-first radix select on order-preserving 64-bit keys of
+// the fp64 values (integer LDS histograms, so the result does not depend on
+// scheduling); equal values are taken in ascending block order; selected
+// blocks are compacted in ascending order.
+#pragma once
+
+#include "sw_common.h"
+
+namespace sw {
+
+constexpr int kMaxPerThread = SW_MAX_BLOCKS / 256;
+
+__device__ __forceinline__ int row_budget_dev(int avail, int nf, int k, int pct) {
+  int t = (k > 0) ? k : (avail * pct + 99) / 100;
+  t = max(t, nf);
+  return min(t, avail);
+}
+
+// This thread's values of a row: v[e] = vals[t*E + e] for the blocks it owns
+// (E = ceil(avail / 256); entries e >= E are never used). The loads carry no
+// condition (the index is clamped into the row), so all of them are in
+// flight before the first value is used.
+__device__ __forceinline__ void load_row_vals(const double* __restrict__ vals, int avail,
+                                              double (&v)[kMaxPerThread]) {
+  const int t = threadIdx.x;
+  const int E = (avail + 255) / 256;
+#pragma unroll
+  for (int e = 0; e < kMaxPerThread; ++e) v[e] = vals[min(t * E + e, avail - 1)];
+}
+
+// Selects from the row held as per-thread values v (as load_row_vals lays
+// them out) with forced set {first, last} (-1 = none).
+__device__ __forceinline__ void select_row_vals(const double (&v)[kMaxPerThread], int avail,
+                                                int first, int last, int k, int pct,
+                                                int32_t* __restrict__ out,
+                                                int32_t* __restrict__ cnt, int kmax) {
+  __shared__ int hist[256];
+  __shared__ int scan_tmp[256];
+  __shared__ int sh_digit, sh_need, sh_cnt;
+  const int t = threadIdx.x;
+  const int E = (avail + 255) / 256;
+  const int nf = (first >= 0) + (last >= 0 && last != first);
+  const int tau = row_budget_dev(avail, nf, k, pct);
+  const int m = tau - nf;                 // ranked blocks to take
+  const int nc = avail - nf;              // ranked candidates
+
+  unsigned long long key[kMaxPerThread];
+  uint32_t candmask = 0, forcedmask = 0;
+#pragma unroll
+  for (int e = 0; e < kMaxPerThread; ++e) {
+    key[e] = 0ull;
+    const int j = t * E + e;
+    if (e < E && j < avail) {
+      if (j == first || j == last) {
+        forcedmask |= 1u << e;
+      } else {
+        candmask |= 1u << e;
+        key[e] = order_key(v[e]);
+      }
+    }
+  }
+
+  // Radix select of the m-th largest candidate key, MSB first. After each
+  // pass the candidates matching `prefix` under `pmask` contain the boundary;
+  // the loop stops early once every candidate in the boundary bin is taken.
+  unsigned long long prefix = 0ull, pmask = 0ull;
+  int need = m;
+  bool take_all_eq = false;
+  const bool partial = (m > 0 && m < nc);
+  if (partial) {
+    for (int pass = 0; pass < 8; ++pass) {
+      const int shift = 56 - 8 * pass;
+      hist[t] = 0;
+      __syncthreads();
+#pragma unroll
+      for (int e = 0; e < kMaxPerThread; ++e)
+        if ((candmask >> e) & 1u)
+          if ((key[e] & pmask) == prefix) atomicAdd(&hist[(int)((key[e] >> shift) & 255ull)], 1);
+      __syncthreads();
+      const int v = hist[255 - t];
+      int total;
+      const int excl = block_exclusive_scan_256(v, scan_tmp, &total);
+      if (v > 0 && excl < need && need <= excl + v) {
+        sh_digit = 255 - t;
+        sh_need = need - excl;
+        sh_cnt = v;
+      }
+      __syncthreads();
+      prefix |= ((unsigned long long)sh_digit) << shift;
+      pmask |= 255ull << shift;
+      need = sh_need;
+      const bool done = (sh_need == sh_cnt);
+      __syncthreads();
+      if (done) {
+        take_all_eq = true;
+        break;
+      }
+    }
+  }
+
+  // rank of each boundary-valued candidate among equals, in index order
+  int my_eq = 0;
+  if (partial && !take_all_eq) {
+#pragma unroll
+    for (int e = 0; e < kMaxPerThread; ++e)
+      if (((candmask >> e) & 1u) && (key[e] & pmask) == prefix) ++my_eq;
+  }
+  int dummy;
+  int eq_before = block_exclusive_scan_256(my_eq, scan_tmp, &dummy);
+
+  uint32_t selmask = forcedmask;
+#pragma unroll
+  for (int e = 0; e < kMaxPerThread; ++e) {
+    if ((candmask >> e) & 1u) {
+      bool take;
+      const unsigned long long kk = key[e] & pmask;
+      if (m >= nc) take = true;
+      else if (m <= 0) take = false;
+      else if (kk > prefix) take = true;
+      else if (kk == prefix) take = take_all_eq || (eq_before++ < need);
+      else take = false;
+      if (take) selmask |= 1u << e;
+    }
+  }
+  const int mine = __popc(selmask);
+  int total_sel;
+  int pos = block_exclusive_scan_256(mine, scan_tmp, &total_sel);
+#pragma unroll
+  for (int e = 0; e < kMaxPerThread; ++e)
+    if ((selmask >> e) & 1u) out[pos++] = t * E + e;
+  for (int q = tau + t; q < kmax; q += 256) out[q] = -1;
+  if (t == 0) *cnt = tau;
+}
+
+// Selects from vals[0..avail) with forced set {first, last} (-1 = none).
+__device__ __forceinline__ void select_row_dev(const double* __restrict__ vals, int avail, int first,
+                                               int last, int k, int pct, int32_t* __restrict__ out,
+                                               int32_t* __restrict__ cnt, int kmax) {
+  double v[kMaxPerThread];
+  load_row_vals(vals, avail, v);
+  select_row_vals(v, avail, first, last, k, pct, out, cnt, kmax);
+}
+
+}  // namespace sw

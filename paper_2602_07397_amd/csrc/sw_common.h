@@ -96,4 +96,45 @@ __device__ __forceinline__ int block_exclusive_scan_256(int v, int* tmp, int* to
   return before + x - v;
 }
 
+__device__ __forceinline__ void butterfly(double& a, double& b) {
+  const double u = a, v = b;
+  a = u + v;
+  b = u - v;
+}
+
+// Unnormalised Walsh-Hadamard transform (natural order) of x[0..d) in LDS by
+// one whole wavefront. Lane l holds elements l*E .. l*E + E - 1 with
+// E = d / 64 (one element in lanes l < d when d < 64); stages of stride
+// below E run inside the lane, the others exchange with lane l ^ (stride/E):
+// the lane holding the lower index keeps u + v, the other u - v. The stages
+// run in the order 1, 2, 4, ... as in the textbook iteration.
+__device__ __forceinline__ void wave_fwht(double* x, int d) {
+  const int lane = threadIdx.x & 63;
+  const int E = d >= 64 ? d / 64 : 1;    // 1, 2 or 4 (d <= 256)
+  double v[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) v[e] = (e < E && lane * E + e < d) ? x[lane * E + e] : 0.0;
+  if (E >= 2) {                          // stride 1 inside the lane
+    butterfly(v[0], v[1]);
+    if (E == 4) butterfly(v[2], v[3]);
+  }
+  if (E == 4) {                          // stride 2 inside the lane
+    butterfly(v[0], v[2]);
+    butterfly(v[1], v[3]);
+  }
+  for (int len = E; len < d; len <<= 1) {
+    const int lx = len / E;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      if (e < E) {
+        const double o = __shfl_xor(v[e], lx);
+        v[e] = (lane & lx) ? (o - v[e]) : (v[e] + o);
+      }
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < 4; ++e)
+    if (e < E && lane * E + e < d) x[lane * E + e] = v[e];
+}
+
 }  // namespace sw

@@ -11,12 +11,18 @@ namespace sw {
 // Byte layout of one layer's decode state (every section 256-byte aligned):
 //   double A_scale[batch]        score scale c frozen at its prefill value
 //   int32  col0[batch]           first key block whose column decode fills
-//   int32  cnt[batch][2]         token counts of the open query / key block
-//   double bar[batch][2][d]      running means of the open query / key block
+//   int32  cnt[batch][2][2]      token counts of the open query / key block,
+//                                two copies selected by the position's parity
+//   double bar[batch][2][2][d]   running means of the open query / key block,
+//                                two copies selected by the position's parity
 //   double qt[batch][r]          sketch of the current token's query
 //   double Qs[batch][b_max][r]   sketch of every query-block representative
 //   double Ks[batch][b_max][r]   sketch of every key-block representative
 //   float  A[batch][b_max][lda]  block-score cache, lda = b_max rounded up to 4
+// The step at position p reads the open-block means and counts of copy
+// (p + 1) % 2 (written by the step at p - 1) and writes copy p % 2, so every
+// workgroup of a step reads the previous values while one of them writes
+// the new ones.
 struct DecodeLayout {
   int64_t scale, col0, cnt, bar, qt, qs, ks, a, total;
   int lda;
@@ -27,14 +33,14 @@ __host__ __device__ inline DecodeLayout decode_layout(int batch, int d, int r, i
   DecodeLayout L;
   L.lda = (b_max + 3) & ~3;
   int64_t o = 0;
-  L.scale = o; o = al(o + 8LL * batch);
-  L.col0 = o;  o = al(o + 4LL * batch);
-  L.cnt = o;   o = al(o + 8LL * batch);
-  L.bar = o;   o = al(o + 16LL * batch * d);
-  L.qt = o;    o = al(o + 8LL * batch * r);
-  L.qs = o;    o = al(o + 8LL * batch * b_max * r);
-  L.ks = o;    o = al(o + 8LL * batch * b_max * r);
-  L.a = o;     o = al(o + 4LL * batch * b_max * L.lda);
+  L.scale = o;  o = al(o + 8LL * batch);
+  L.col0 = o;   o = al(o + 4LL * batch);
+  L.cnt = o;    o = al(o + 16LL * batch);
+  L.bar = o;    o = al(o + 32LL * batch * d);
+  L.qt = o;     o = al(o + 8LL * batch * r);
+  L.qs = o;     o = al(o + 8LL * batch * b_max * r);
+  L.ks = o;     o = al(o + 8LL * batch * b_max * r);
+  L.a = o;      o = al(o + 4LL * batch * b_max * L.lda);
   L.total = o;
   return L;
 }
@@ -77,16 +83,23 @@ hipError_t launch_decode_sketch(int dtype, const void* q_new, const void* k_new,
                                 hipStream_t st, const void* v_new = nullptr, void* Kc = nullptr,
                                 void* Vc = nullptr, int T_max = 0);
 
+// Alg. 2 step 5 for the per-layer entry point: the walk row of every
+// sequence, divided by its largest magnitude, into r_out [batch][b_max].
 hipError_t launch_decode_walk(const char* state, int batch, int d, int r, int b_max, int B,
                               const int32_t* pos, int s_exp, bool relu, const double* r_prev,
-                              double* r_out, hipStream_t st, bool normalize = true);
+                              double* r_out, hipStream_t st);
 
-// normalize: first divide each row (in place) by its largest magnitude over
-// blocks 0..b_cur and zero the rest, as the walk row's normalisation does.
+// Alg. 2 steps 5-6 for the one-call decode step: the same walk row written to
+// rows [batch][b_max], normalised by the selection kernel, which then selects.
+hipError_t launch_decode_walk_select(const char* state, int batch, int d, int r, int b_max, int B,
+                                     const int32_t* pos, int s_exp, bool relu,
+                                     const double* r_prev, double* rows, int k, int pct,
+                                     uint32_t flags, int32_t* idx, int32_t* cnt, int kmax,
+                                     hipStream_t st);
+
 hipError_t launch_select_decode(const double* rows, int batch, int b_max, int B,
                                 const int32_t* pos, int k, int pct, uint32_t flags, int32_t* idx,
-                                int32_t* cnt, int kmax, hipStream_t st,
-                                double* normalize_rows = nullptr);
+                                int32_t* cnt, int kmax, hipStream_t st);
 
 int decode_attn_splits(int batch, int h_kv);
 
