@@ -325,6 +325,26 @@ int sw_sparse_attn_decode(int dtype, const void* q, const void* Kc, const void* 
                           void* workspace, int64_t workspace_bytes, void* stream);
 
 /*
+ * sw_sparse_attn_decode_noalloc - sw_sparse_attn_decode for callers that
+ * cannot allocate device memory (code under HIP graph capture, serving loops
+ * that forbid allocation): the same kernels and results, with the split-K
+ * partials in a fixed device array of SW_NOALLOC_SCRATCH_BYTES that the
+ * library holds on each GPU it runs on until the process ends, instead of a
+ * caller workspace. The call allocates nothing. A call whose partials need
+ * more than SW_NOALLOC_SCRATCH_BYTES (sw_decode_attn_workspace_bytes) returns
+ * SW_ERR_INVALID_ARG. Every call on one GPU shares that GPU's array: calls
+ * that overlap on one GPU (different streams or threads) race; calls in
+ * stream order do not. The array needs no clearing: each call writes every
+ * partial it reads. The first call on a device looks the array's address up
+ * once. Other arguments as in sw_sparse_attn_decode.
+ */
+#define SW_NOALLOC_SCRATCH_BYTES (8 * 1024 * 1024)
+int sw_sparse_attn_decode_noalloc(int dtype, const void* q, const void* Kc, const void* Vc,
+                                  int batch, int h_q, int h_kv, int d, int T_max, int B,
+                                  const int32_t* pos, const int32_t* idx, const int32_t* cnt,
+                                  int kmax, float scale, void* O, void* stream);
+
+/*
  * sw_decode_step - one decode step of every layer in one call: Alg. 2 steps
  * 1-7 for layer 0, 1, ..., layers-1 in order (the walk row of layer l starts
  * from that of layer l-1; layer 0 is the first walked layer). Per layer it

@@ -76,7 +76,12 @@ _SIGNATURES = {
     "sw_sparse_attn_decode": (_c_int, [_c_int, _vp, _vp, _vp, _c_int, _c_int, _c_int, _c_int, _c_int,
                                        _c_int, _vp, _vp, _vp, _c_int, ctypes.c_float, _vp, _vp, _c_i64,
                                        _vp]),
+    "sw_sparse_attn_decode_noalloc": (_c_int, [_c_int, _vp, _vp, _vp, _c_int, _c_int, _c_int, _c_int,
+                                               _c_int, _c_int, _vp, _vp, _vp, _c_int, ctypes.c_float,
+                                               _vp, _vp]),
 }
+
+NOALLOC_SCRATCH_BYTES = 8 * 1024 * 1024
 
 _lib = None
 
@@ -431,6 +436,28 @@ def sparse_attn_decode(q: torch.Tensor, Kc: torch.Tensor, Vc: torch.Tensor, B: i
                                       float(scale), _dev(O, "O"), _dev(workspace, "workspace"),
                                       workspace.numel(), _stream(dev))
     _check(rc, "sw_sparse_attn_decode")
+    return O
+
+
+def sparse_attn_decode_noalloc(q: torch.Tensor, Kc: torch.Tensor, Vc: torch.Tensor, B: int,
+                               pos: torch.Tensor, idx: torch.Tensor, cnt: torch.Tensor, kmax: int,
+                               scale: float = 0.0, O: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """sparse_attn_decode without a workspace: the library's fixed per-GPU
+    scratch holds the split-K partials (pass a pre-allocated ``O`` to make
+    the whole call allocation-free)."""
+    batch, h_q, d = q.shape
+    _, h_kv, T_max, _ = Kc.shape
+    if O is None:
+        O = torch.empty_like(q)
+    if not (Kc.dtype == Vc.dtype == q.dtype == O.dtype):
+        raise SketchWalkError("q, Kc, Vc, O must share a dtype")
+    rc = load().sw_sparse_attn_decode_noalloc(_dtype_code(q), _dev(q, "q"), _dev(Kc, "Kc"),
+                                              _dev(Vc, "Vc"), batch, h_q, h_kv, d, T_max, B,
+                                              _dev(pos, "pos", torch.int32),
+                                              _dev(idx, "idx", torch.int32),
+                                              _dev(cnt, "cnt", torch.int32), kmax, float(scale),
+                                              _dev(O, "O"), _stream(q.device))
+    _check(rc, "sw_sparse_attn_decode_noalloc")
     return O
 
 

@@ -475,6 +475,24 @@ int sw_sparse_attn_decode(int dtype, const void* q, const void* Kc, const void* 
   return hip_status(e, "sw_sparse_attn_decode launch");
 }
 
+int sw_sparse_attn_decode_noalloc(int dtype, const void* q, const void* Kc, const void* Vc,
+                                  int batch, int h_q, int h_kv, int d, int T_max, int B,
+                                  const int32_t* pos, const int32_t* idx, const int32_t* cnt,
+                                  int kmax, float scale, void* O, void* stream) {
+  const int64_t need = sw_decode_attn_workspace_bytes(batch, h_q, h_kv, d);
+  if (need < 0) return SW_ERR_INVALID_ARG;
+  if (need > (int64_t)SW_NOALLOC_SCRATCH_BYTES)
+    return fail(SW_ERR_INVALID_ARG,
+                "batch=%d h_q=%d d=%d needs %lld bytes of split-K scratch, more than the %lld "
+                "bytes the allocation-free entry point holds (use sw_sparse_attn_decode)",
+                batch, h_q, d, (long long)need, (long long)SW_NOALLOC_SCRATCH_BYTES);
+  void* ws = nullptr;
+  hipError_t e = sw::noalloc_scratch(&ws);
+  if (e != hipSuccess) return hip_status(e, "sw_sparse_attn_decode_noalloc scratch lookup");
+  return sw_sparse_attn_decode(dtype, q, Kc, Vc, batch, h_q, h_kv, d, T_max, B, pos, idx, cnt, kmax,
+                               scale, O, ws, need, stream);
+}
+
 int64_t sw_decode_step_workspace_bytes(int batch, int h_q, int h_kv, int d) {
   return sw_decode_attn_workspace_bytes(batch, h_q, h_kv, d);
 }

@@ -11,6 +11,8 @@
 //                           G query heads of the group with 16-byte loads and
 //                           keeps an online softmax per (key lane group, head)
 //  attn_merge_kernel        log-sum-exp merge of the splits
+#include <mutex>
+
 #include "sw_common.h"
 #include "sw_internal.h"
 
@@ -537,6 +539,38 @@ static void launch_attn_decode_t(int G, dim3 grid, hipStream_t st, const T* q, c
     case 4: hipLaunchKernelGGL((attn_decode_kernel<T, D, 4>), grid, dim3(256), 0, st, q, Kc, Vc, h_kv, T_max, B, pos, idx, cnt, kmax, sl2, S, ws); break;
     default: hipLaunchKernelGGL((attn_decode_kernel<T, D, 8>), grid, dim3(256), 0, st, q, Kc, Vc, h_kv, T_max, B, pos, idx, cnt, kmax, sl2, S, ws); break;
   }
+}
+
+// ---------------------------------------------------------------------------
+// fixed scratch for the allocation-free entry point
+// ---------------------------------------------------------------------------
+
+// The split-K partials of sw_sparse_attn_decode_noalloc: a fixed device array
+// (each GPU the library runs on holds its own copy until the process ends).
+// Host code never passes the array's name to a kernel; it passes the device
+// address looked up below, once per device.
+static __device__ __align__(256) __attribute__((used)) float scratch[SW_NOALLOC_SCRATCH_BYTES / 4];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices];        // device address of `scratch`, per device
+}  // namespace
+
+hipError_t noalloc_scratch(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return hipSuccess;
 }
 
 hipError_t launch_attn_decode(int dtype, const void* q, const void* Kc, const void* Vc, int batch,

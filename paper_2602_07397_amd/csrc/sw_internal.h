@@ -103,6 +103,10 @@ hipError_t launch_select_decode(const double* rows, int batch, int b_max, int B,
 
 int decode_attn_splits(int batch, int h_kv);
 
+// Device address of this device's fixed scratch array
+// (SW_NOALLOC_SCRATCH_BYTES), looked up on the first call on each device.
+hipError_t noalloc_scratch(void** out);
+
 hipError_t launch_attn_decode(int dtype, const void* q, const void* Kc, const void* Vc, int batch,
                               int h_q, int h_kv, int d, int T_max, int B, const int32_t* pos,
                               const int32_t* idx, const int32_t* cnt, int kmax, float scale,

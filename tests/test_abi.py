@@ -169,3 +169,13 @@ def test_header_compiles_and_links_from_c(tmp_path, lang):
     assert int(r["step_ws"]) > 0
     assert r["bad_variant"].startswith("1 ") and "variant" in r["bad_variant"]
     assert r["too_many_blocks"] == "2"
+
+
+def test_noalloc_decode_attention_refuses_oversize_calls_on_the_host():
+    """A call whose split-K partials exceed the fixed scratch is refused
+    before any device work (no GPU needed to see it)."""
+    batch, h_q, h_kv, d = 4096, 32, 8, 128
+    assert sw.decode_attn_workspace_bytes(batch, h_q, h_kv, d) > sw.NOALLOC_SCRATCH_BYTES
+    rc, msg = _err("sw_sparse_attn_decode_noalloc", sw.SW_BF16, FAKE, FAKE, FAKE, batch, h_q, h_kv,
+                   d, 4096, 64, FAKE, FAKE, FAKE, 8, ctypes.c_float(0.0), FAKE, None)
+    assert rc == 1 and "scratch" in msg, msg
