@@ -13,6 +13,12 @@ alone: its algorithmic FLOPs per launch over its average launch time measured
 with HIP events on the launch stream, against the bf16 dense MFMA peak.
 ``cpu_baseline`` is the fp64 oracle timed on a bounded sample of the same
 layer on this host's cores.
+
+The same line carries the decode workload (``decode``: tok/s, the attention
+kernel's roofline and the whole step's HBM fraction), the other prefill
+workloads (``configs``: the 131072-token layer at 10/20/40/100% and the
+variable-length batch) and the sparse/dense ratios at 16K-128K tokens
+(``speedup``); ``--no-extras`` leaves out the last two.
 """
 from __future__ import annotations
 
@@ -78,10 +84,26 @@ def attention_flops(idx: np.ndarray, cnt: np.ndarray, cu, B: int, h_q: int, d: i
     return 4 * d * h_q * alg, 4 * d * h_q * tile
 
 
-def cpu_baseline(Qh, Kh, Vh, cu, B, signs, cols, s, pct, pairs, seed=0):
+def host_cpu_model() -> str:
+    """The host CPU's model name (as lscpu reports it)."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
+
+
+def cpu_baseline(Qh, Kh, Vh, cu, B, signs, cols, s, pct, pairs, needle_blocks=(), seed=0):
     """Times the fp64 oracle on one layer: the full selection path (sketch,
-    walk, select) plus masked attention on `pairs` random (head, query block)
-    pairs; the attention time is scaled to the whole layer."""
+    walk, select) plus masked attention on a stratified sample of `pairs`
+    (head, query block) pairs: every head of the query blocks that hold a
+    planted needle's query, every head of the first and the last block, the
+    rest drawn at random; the attention time is scaled to the whole layer by
+    the executed FLOPs."""
     import oracle as O
     try:
         from threadpoolctl import threadpool_info
@@ -101,7 +123,10 @@ def cpu_baseline(Qh, Kh, Vh, cu, B, signs, cols, s, pct, pairs, seed=0):
     h_q = Q.shape[0]
     b = len(sel)
     rng = np.random.default_rng(seed)
-    samp = [(int(rng.integers(h_q)), int(rng.integers(b))) for _ in range(pairs)]
+    strata = sorted({int(i) for i in needle_blocks if 0 <= int(i) < b} | {0, b - 1})
+    samp = [(u, i) for i in strata for u in range(h_q)]
+    n_fixed = len(samp)
+    samp += [(int(rng.integers(h_q)), int(rng.integers(b))) for _ in range(max(0, pairs - n_fixed))]
     t0 = time.perf_counter()
     flops_s = 0
     n = Q.shape[1]
@@ -125,11 +150,13 @@ def cpu_baseline(Qh, Kh, Vh, cu, B, signs, cols, s, pct, pairs, seed=0):
         "value": flops_layer / t_layer / 1e12,
         "unit": "TFLOP/s",
         "cores": int(cores),
+        "cpu_model": host_cpu_model(),
         "kind": "oracle",
         "sample": (f"layer 0 of the workload: full fp64 selection path ({t_sel:.1f} s) + masked "
-                   f"attention on {pairs} random (head, query-block) pairs of {total_pairs} "
-                   f"({t_attn:.1f} s), attention time scaled by executed FLOPs to the layer; "
-                   f"input conversion ({t_conv:.1f} s) excluded"),
+                   f"attention on {len(samp)} (head, query-block) pairs of {total_pairs}: every "
+                   f"head of the needle query blocks and of blocks 0 and b-1 ({n_fixed} pairs), "
+                   f"the rest random ({t_attn:.1f} s); attention time scaled by executed FLOPs "
+                   f"to the layer; input conversion ({t_conv:.1f} s) excluded"),
         "layer_seconds_extrapolated": t_layer,
     }
 
@@ -193,6 +220,7 @@ def cpu_baseline_decode(budget_s: float = 10.0, layers: int = 4, seed: int = 0) 
         "value": w.batch / step_s,
         "unit": "tok/s",
         "cores": int(cores),
+        "cpu_model": host_cpu_model(),
         "kind": "oracle",
         "sample": (f"one sequence, {layers} layers x {done // layers} steps of the decode workload's "
                    f"shapes (65536-token caches, b_max {b_max}): {t_layer_step * 1e3:.0f} ms per "
@@ -1062,6 +1090,8 @@ def main() -> int:
     ap.add_argument("--cpu-pairs", type=int, default=3000)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-decode", action="store_true")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="skip the stress/varlen workloads and the sparse/dense ratios")
     ap.add_argument("--decode-steps", type=int, default=256)
     ap.add_argument("--decode-layers", type=int, default=None, help="override (debug only)")
     ap.add_argument("--decode-eager", action="store_true", help="launch the decode step eagerly")
@@ -1125,6 +1155,13 @@ def main() -> int:
         torch.cuda.empty_cache()
     if args.only != "prefill" and not args.no_decode:
         out["decode"] = run_decode(args, dev)
+        torch.cuda.empty_cache()
+    if args.only is None and not args.no_extras:
+        # the other workloads and the sparse/dense ratios, measured in the same run
+        out["configs"] = run_configs(args, dev)["prefill"]
+        torch.cuda.empty_cache()
+        out["speedup"] = run_speedup(args, dev)
+        torch.cuda.empty_cache()
     if "decode" in out and args.only != "decode" and not args.no_cpu_baseline:
         print("[bench] timing the oracle's decode on the host", file=sys.stderr, flush=True)
         out["decode"]["cpu_baseline"] = cpu_baseline_decode()
@@ -1133,8 +1170,9 @@ def main() -> int:
         w = synth.WORKLOADS["llama8b"]
         signs, cols = synth.srht_params(w.d, w.r, w.seed)
         print("[bench] timing the oracle on the host", file=sys.stderr, flush=True)
+        needles = [p // w.B for (_, p) in synth.needle_plan(w, 0)[0]]
         out["cpu_baseline"] = cpu_baseline(*cpu_layer, synth.cu_seqlens(w.seqlens), w.B, signs, cols,
-                                           w.s, w.pct, args.cpu_pairs)
+                                           w.s, w.pct, args.cpu_pairs, needle_blocks=needles)
     print(json.dumps(out), flush=True)
     return 0
 

@@ -74,3 +74,22 @@ def test_more_than_one_gpu_is_refused():
                          capture_output=True, text=True, timeout=120)
     assert res.returncode == 2
     assert "one GPU" in res.stderr or "one GPU" in res.stdout
+
+
+def test_decode_step_bytes_follow_the_selection_rule():
+    """The decode byte count takes tau - 1 whole earlier blocks and the
+    current block's tokens up to p (tau from the oracle's budget rule with the
+    first and current blocks forced), and the score-cache entries of the lower
+    triangle plus the decode-filled columns."""
+    import oracle as O
+    B, h_q, h_kv, d, r, pct = 64, 32, 8, 128, 64, 20
+    for n0, p in ((65536, 65536), (65536, 65600), (65532, 65533), (100, 130)):
+        got = bench.decode_step_bytes(p, n0, B, h_q, h_kv, d, r, pct)
+        bc = p // B
+        tau = O.row_budget(bc + 1, len(O.forced_set(bc, O.FORCE_BOTH)), pct=pct)
+        toks = (tau - 1) * B + (p - bc * B + 1)
+        assert got["kv"] == toks * h_kv * d * 2 * 2
+        col0 = n0 // B
+        entries = sum(1 for m in range(bc + 1) for j in range(bc + 1) if j <= m or j >= col0)
+        assert got["walk"] == entries * 4
+        assert got["sketch"] == 2 * bc * r * 8

@@ -15,7 +15,8 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 def test_bench_line_has_the_contract_fields():
     res = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--steps", "1",
-                          "--warmup", "1", "--decode-steps", "4", "--cpu-pairs", "20"],
+                          "--warmup", "1", "--decode-steps", "4", "--cpu-pairs", "300",
+                          "--speedup-lengths", "16384"],
                          capture_output=True, text=True, timeout=600, cwd=ROOT)
     assert res.returncode == 0, res.stderr[-2000:]
     line = res.stdout.strip().splitlines()[-1]
@@ -39,3 +40,13 @@ def test_bench_line_has_the_contract_fields():
     assert drl["bound"] == "hbm" and drl["unit"] == "GB/s" and drl["peak"] == 8000.0
     assert drl["frac"] == pytest.approx(drl["achieved"] / drl["peak"], rel=1e-3)
     assert dec["cpu_baseline"]["kind"] == "oracle" and dec["cpu_baseline"]["unit"] == "tok/s"
+    assert cb["cpu_model"] and dec["cpu_baseline"]["cpu_model"]
+    hs = dec["hbm_step"]
+    assert hs["unit"] == "GB/s" and hs["frac"] == pytest.approx(hs["achieved"] / hs["peak"], rel=1e-3)
+    assert sum(hs["share"].values()) == pytest.approx(1.0, abs=1e-3)
+    # the other workloads and the sparse/dense ratios come in the same line
+    pcts = sorted(r["density_pct"] for r in d["configs"] if r["workload"] == "stress")
+    assert pcts == [10, 20, 40, 100]
+    assert any(r["workload"] == "varlen" for r in d["configs"])
+    assert d["speedup"]["prefill_one_layer"][0]["speedup_vs_dense_this_kernel"] > 1.0
+    assert d["speedup"]["decode_one_layer"][0]["speedup_vs_dense_this_kernel"] > 1.0
