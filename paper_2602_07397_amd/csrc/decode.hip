@@ -18,7 +18,9 @@
 //                         score cache; one workgroup per (sequence, pair of
 //                         32-column strips), the pairs balanced so that every
 //                         workgroup reads about as many rows, 32 row groups
-//                         reduced in LDS in a fixed order
+//                         reduced in LDS in a fixed order; the rows above a
+//                         strip, which hold only its decode-filled columns,
+//                         are shared by every thread of the workgroup
 //  walk_row_norm_kernel   divides the row by its largest magnitude (the
 //                         one-call step does this in select_decode_norm_kernel
 //                         before selecting, step 6)
@@ -328,7 +330,7 @@ constexpr int kStripQuads = kStripCols / 4;
 constexpr int kStripGroups = SW_STRIP_GROUPS;
 constexpr int kStripThreads = kStripQuads * kStripGroups;
 #ifndef SW_STRIP_ROWS
-#define SW_STRIP_ROWS 10                 // rows each thread loads before adding
+#define SW_STRIP_ROWS 4                  // rows each thread loads before adding
 #endif
 constexpr int kStripBufWord3 = 0x00020000;   // raw buffer descriptor word 3 (gfx9 family)
 
@@ -344,20 +346,28 @@ __device__ __forceinline__ double walk_weight(float a, double inv_c, int s_exp) 
   }
 }
 
+__device__ __forceinline__ uint4 load_quad(__amdgpu_buffer_rsrc_t ra, int off) {
+  return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(ra, off, 0, 0));
+}
+
 // One workgroup per (sequence, strip pair): strips k and S-1-k of 32 columns
-// (S = ceil(lda / 32)), so that every workgroup reads about b_cur rows in all.
-// Strip x needs the rows m >= 32 x (the causal part), or every row when decode
-// filled one of its columns (col0 <= j <= b_cur). The row groups are shared
-// between the two strips in proportion to their row counts; thread (row
-// group g, column quad q) takes every n-th row of its strip (n = the strip's
-// group count), 16-byte loads of 4 columns, a row of a strip being one
-// 128-byte piece. r_out[j] = sum over those rows m (per group ascending, then
-// over the strip's groups in blocks of 8, then over the blocks, each in
-// order) of r_prev[m] W[m][j]. Entries the score cache
-// holds as zero (above the diagonal outside the decode-filled columns, past
-// b_cur) give zero terms, so no per-element mask is needed; quads that are
-// wholly zero are not loaded. At the first walked layer (r_prev NULL) the
-// row of W itself, r_out[j] = W[b_cur][j]. Entries past b_cur are 0.
+// (S = ceil(lda / 32)). Strip x's causal part is the rows m = 32 x .. b_cur
+// (every column of the strip can be non-zero there), so a pair holds about
+// b_cur rows in all. Its row groups are shared between the two strips in
+// proportion to their row counts; thread (row group g, column quad q) takes
+// every n-th row of its strip (n = the strip's group count) with 16-byte
+// loads of 4 columns, a row of a strip being one 128-byte piece. The columns
+// decode filled (col0 .. b_cur) are non-zero in the rows above the strip as
+// well (m < 32 x): those rows hold nothing else in the strip, so every thread
+// of the workgroup takes a share of them, for those columns only.
+// r_out[j] = (sum over the causal rows: per group ascending, then over the
+// strip's groups in blocks of 8, then over the blocks) + (sum over the rows
+// above: per thread ascending, then over the threads in blocks of 16, then
+// over the blocks) of r_prev[m] W[m][j]. Entries the score cache holds as
+// zero (above the diagonal outside the decode-filled columns, past b_cur)
+// give zero terms; quads that are wholly zero are not loaded. At the first
+// walked layer (r_prev NULL) the row of W itself, r_out[j] = W[b_cur][j].
+// Entries past b_cur are 0.
 template <bool S8, bool RELU>
 __global__ __launch_bounds__(kStripThreads) void walk_strip_kernel(const char* __restrict__ state,
                                                                    int batch, int d, int r,
@@ -366,10 +376,15 @@ __global__ __launch_bounds__(kStripThreads) void walk_strip_kernel(const char* _
                                                                    int s_exp,
                                                                    const double* __restrict__ r_prev,
                                                                    double* __restrict__ r_out) {
-  // the walk row of the previous layer during the row loop, then the row
-  // groups' sums (both fit: b_max <= 4096 <= kStripGroups * kStripCols)
-  __shared__ double smem[kStripGroups * kStripCols > SW_MAX_BLOCKS ? kStripGroups * kStripCols
-                                                                   : SW_MAX_BLOCKS];
+  // the walk row of the previous layer during the row loops, then the row
+  // groups' sums (both fit: b_max <= 4096 <= kStripGroups * kStripCols * 4)
+  constexpr int kSmem = kStripGroups * kStripCols > SW_MAX_BLOCKS ? kStripGroups * kStripCols
+                                                                  : SW_MAX_BLOCKS;
+  __shared__ double smem[kSmem];
+  __shared__ double red2[2][kStripGroups / 8][kStripCols];
+  __shared__ double xr[kStripThreads][4];
+  __shared__ double xred[kStripThreads / 16][4];
+  __shared__ double xsum[2][kStripCols];
   const DecodeLayout L = decode_layout(batch, d, r, b_max);
   const int lda = L.lda;
   const int bi = blockIdx.x;
@@ -398,13 +413,8 @@ __global__ __launch_bounds__(kStripThreads) void walk_strip_kernel(const char* _
   const double inv_c = 1.0 / (c0 > 0.0 ? c0 : 1.0);
   const float* A = reinterpret_cast<const float*>(state + L.a) + (long long)bi * b_max * lda;
   const int q = t % kStripQuads, g = t / kStripQuads;
-  auto first_row = [&](int x) {
-    const int j0 = x * kStripCols;
-    return (j0 + kStripCols - 1 >= col0) ? 0 : j0;
-  };
-  const int ma = first_row(sa), mb = first_row(sb);
-  const int na = (sa * kStripCols <= bc) ? bc - ma + 1 : 0;
-  const int nbr = (sb != sa && sb * kStripCols <= bc) ? bc - mb + 1 : 0;
+  const int na = (sa * kStripCols <= bc) ? bc - sa * kStripCols + 1 : 0;
+  const int nbr = (sb != sa && sb * kStripCols <= bc) ? bc - sb * kStripCols + 1 : 0;
   const int total = na + nbr;
   // row groups of strip a: about kStripGroups * na / total (each strip with
   // rows gets at least one)
@@ -415,10 +425,15 @@ __global__ __launch_bounds__(kStripThreads) void walk_strip_kernel(const char* _
   const int x = in_a ? sa : sb;
   const int gi = in_a ? g : g - ga;                 // group index within the strip
   const int ng = in_a ? ga : kStripGroups - ga;     // groups of the strip
-  const int m0 = in_a ? ma : mb;
+  const int m0 = x * kStripCols;
   const int nrows = in_a ? na : nbr;
   const int j = x * kStripCols + 4 * q;             // this thread's 4 columns
   const bool okj = j <= bc;                          // the quad holds a block
+  // the sequence's score cache as a buffer: 32-bit offsets, and a load whose
+  // quad holds nothing is sent past the end (it reads zeros)
+  const int bytes = b_max * lda * 4;
+  const __amdgpu_buffer_rsrc_t ra =
+      __builtin_amdgcn_make_buffer_rsrc((void*)A, (short)0, bytes, kStripBufWord3);
   double acc[4] = {0.0, 0.0, 0.0, 0.0};
   if (r_prev == nullptr) {
     if (gi == 0 && nrows > 0 && okj) {
@@ -429,11 +444,7 @@ __global__ __launch_bounds__(kStripThreads) void walk_strip_kernel(const char* _
     }
   } else {
     __syncthreads();                     // the staged row is visible
-    // the sequence's score cache as a buffer: 32-bit offsets, and a load
-    // whose quad holds nothing is sent past the end (it reads zeros)
-    const int bytes = b_max * lda * 4;
-    const __amdgpu_buffer_rsrc_t ra =
-        __builtin_amdgcn_make_buffer_rsrc((void*)A, (short)0, bytes, kStripBufWord3);
+    const double* rp = smem;
     constexpr int NR = S8 ? SW_STRIP_ROWS : SW_STRIP_ROWS / 2;   // the general power needs more registers
     for (int i0 = gi; i0 < nrows; i0 += NR * ng) {
       // every load of the pass is issued before any is used
@@ -441,15 +452,12 @@ __global__ __launch_bounds__(kStripThreads) void walk_strip_kernel(const char* _
 #pragma unroll
       for (int v = 0; v < NR; ++v) {
         const int i = i0 + v * ng;
-        const int m = m0 + min(i, nrows - 1);
-        const bool ok = i < nrows && okj && (j <= m || j + 3 >= col0);
-        const int off = ok ? (m * lda + j) * 4 : bytes;
-        a[v] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(ra, off, 0, 0));
+        const bool ok = i < nrows && okj;
+        a[v] = load_quad(ra, ok ? ((m0 + i) * lda + j) * 4 : bytes);
       }
 #pragma unroll
       for (int v = 0; v < NR; ++v) {
-        const int i = i0 + v * ng;
-        const double rv = smem[m0 + min(i, nrows - 1)];
+        const double rv = rp[m0 + min(i0 + v * ng, nrows - 1)];
         const float av[4] = {__uint_as_float(a[v].x), __uint_as_float(a[v].y),
                              __uint_as_float(a[v].z), __uint_as_float(a[v].w)};
 #pragma unroll
@@ -457,7 +465,63 @@ __global__ __launch_bounds__(kStripThreads) void walk_strip_kernel(const char* _
       }
     }
   }
-  __syncthreads();                       // the previous row is no longer read
+  // the decode-filled columns of each strip over the rows above it
+  // (rows 0 .. 32 x - 1), one quad at a time, every thread a share of rows
+  if (t < 2 * kStripCols) xsum[t / kStripCols][t % kStripCols] = 0.0;
+  __syncthreads();
+  if (r_prev != nullptr) {
+    const double* rp = smem;
+#pragma unroll 1
+    for (int which = 0; which < 2; ++which) {
+      const int xs = which ? sb : sa;
+      if (which == 1 && sb == sa) break;
+      const int xj0 = xs * kStripCols;
+      if (xj0 > bc) continue;
+      const int qlo = max(col0 - xj0, 0) / 4, qhi = min(bc - xj0, kStripCols - 1) / 4;
+      if (xj0 + kStripCols - 1 < col0 || xj0 == 0) continue;
+#pragma unroll 1
+      for (int qd = qlo; qd <= qhi; ++qd) {
+        const int jd = xj0 + 4 * qd;
+        double xa[4] = {0.0, 0.0, 0.0, 0.0};
+        for (int m1 = t; m1 < xj0; m1 += 8 * kStripThreads) {
+          uint4 a[8];
+#pragma unroll
+          for (int v = 0; v < 8; ++v) {
+            const int m = m1 + v * kStripThreads;
+            a[v] = load_quad(ra, m < xj0 ? (m * lda + jd) * 4 : bytes);
+          }
+#pragma unroll
+          for (int v = 0; v < 8; ++v) {
+            const double rv = rp[min(m1 + v * kStripThreads, xj0 - 1)];
+            const float av[4] = {__uint_as_float(a[v].x), __uint_as_float(a[v].y),
+                                 __uint_as_float(a[v].z), __uint_as_float(a[v].w)};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) xa[e] += rv * walk_weight<S8, RELU>(av[e], inv_c, s_exp);
+          }
+        }
+        // fixed-order reduction over the threads: blocks of 16, then the blocks
+#pragma unroll
+        for (int e = 0; e < 4; ++e) xr[t][e] = xa[e];
+        __syncthreads();
+        if (t < (kStripThreads / 16) * 4) {
+          const int bk = t / 4, e = t % 4;
+          double v = 0.0;
+#pragma unroll
+          for (int u = 0; u < 16; ++u) v += xr[bk * 16 + u][e];
+          xred[bk][e] = v;
+        }
+        __syncthreads();
+        if (t < 4) {
+          double v = 0.0;
+#pragma unroll
+          for (int u = 0; u < kStripThreads / 16; ++u) v += xred[u][t];
+          xsum[which][4 * qd + t] = v;
+        }
+        __syncthreads();
+      }
+    }
+  }
+  __syncthreads();
   double* red = smem;                    // [kStripGroups][kStripCols]
 #pragma unroll
   for (int e = 0; e < 4; ++e) red[g * kStripCols + 4 * q + e] = acc[e];
@@ -465,7 +529,6 @@ __global__ __launch_bounds__(kStripThreads) void walk_strip_kernel(const char* _
   // fixed-order reduction over a strip's groups: sums of 8 consecutive groups
   // (one per thread: strip, block of 8 groups, column), then of the blocks
   constexpr int kBlk = kStripGroups / 8;
-  __shared__ double red2[2][kBlk][kStripCols];
   {
     const int which = t / (kBlk * kStripCols), bk = (t / kStripCols) % kBlk, c = t % kStripCols;
     const int g0 = which ? ga : 0, g1 = which ? kStripGroups : ga;
@@ -489,6 +552,7 @@ __global__ __launch_bounds__(kStripThreads) void walk_strip_kernel(const char* _
 #pragma unroll
       for (int u = 0; u < kBlk; ++u) v += vals[u];
       const int jj = xs * kStripCols + c;
+      if (r_prev != nullptr && jj >= col0 && xs * kStripCols > 0) v += xsum[which][c];
       if (jj < b_max) r_out[(long long)bi * b_max + jj] = (jj <= bc) ? v : 0.0;
     }
   }
