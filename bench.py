@@ -46,9 +46,9 @@ PEAK_HBM_GBS = 8000.0
 FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
 MEASURED_TRAFFIC = {
     "attn_prefill.hip": ("2149d18851d90f262dfc6f4961c3e5831781851fa204e37a2fc0bb1999ee0fa0",
-                         334278.8 * 1024, 262144.0 * 1024),
-    "attn_decode.hip": ("e75a2c49d4006ba95d386c0e789150059e2b98497164fdcd8ce9320dd90b1790",
-                        419752.1 * 1024, 1088.0 * 1024),
+                         334347.4 * 1024, 262144.0 * 1024),
+    "attn_decode.hip": ("63befefed809dbbb7d18ce6f2ea196fd42b541d037ae887a09056ecb2c0f901d",
+                        419749.8 * 1024, 1088.0 * 1024),
 }
 
 
