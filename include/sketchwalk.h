@@ -223,8 +223,12 @@ int sw_sparse_attn_prefill(int dtype, const void* Q, const void* K, const void* 
  *   double qt[batch][r]           sketch of the latest token's query
  *   double Qs[batch][b_max][r]    sketch of every query-block representative
  *   double Ks[batch][b_max][r]    sketch of every key-block representative
- *   float  A[batch][b_max][lda]   block-score cache (fp32), lda = b_max rounded
- *                                 up to a multiple of 4
+ *   float  rowc[batch][b_max], colc[batch][b_max]  the open block's score
+ *                                 row and column as the last step wrote them
+ *   float  A[batch][lda/32][b_max][32]  block-score cache (fp32) in strips
+ *                                 of 32 columns: score (m, j) of a sequence
+ *                                 at float offset ((j/32) b_max + m) 32 + j%32,
+ *                                 lda = b_max rounded up to a multiple of 32
  * Checkpointing a decode is a byte copy of this buffer (plus the caches)
  * taken between calls.
  * pos [batch] int32 (device): 0-based position of the new token of each

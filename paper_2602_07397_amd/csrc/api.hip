@@ -562,13 +562,10 @@ int sw_decode_step(int dtype, int layers, int batch, int h_q, int h_kv, int d, i
     double* rl = rows + l * row_step;
     int32_t* il = idx + (int64_t)l * batch * kmax;
     int32_t* cl = cnt + (int64_t)l * batch;
-    hipError_t e = sw::launch_decode_sketch(dtype, qb + l * q_step, kb + l * kv_step, batch, h_q,
-                                            h_kv, d, B, pos, signs, cols, r, b_max, stl, st,
-                                            vb + l * kv_step, Kl, Vl, T_max);
-    if (e == hipSuccess)
-      e = sw::launch_decode_walk_select(stl, batch, d, r, b_max, B, pos, s,
-                                        walk_variant == SW_WALK_RELU, l == 0 ? nullptr : rl - row_step,
-                                        rl, k, density_pct, flags, il, cl, kmax, st);
+    hipError_t e = sw::launch_decode_layer(
+        dtype, qb + l * q_step, kb + l * kv_step, vb + l * kv_step, Kl, Vl, T_max, batch, h_q,
+        h_kv, d, B, pos, signs, cols, r, b_max, stl, s, walk_variant == SW_WALK_RELU,
+        l == 0 ? nullptr : rl - row_step, rl, k, density_pct, flags, il, cl, kmax, st);
     if (e == hipSuccess)
       e = sw::launch_attn_decode(dtype, qb + l * q_step, Kl, Vl, batch, h_q, h_kv, d, T_max, B, pos,
                                  il, cl, kmax, scale, Ob + l * q_step,

@@ -12,18 +12,23 @@
 //                         workgroup writes its rows' entries of (i) the new
 //                         score row and (ii) the new last column, 4 lanes per
 //                         sketch row
-//  walk_strip_kernel      step 5 on the query row only: r = W[b_q, :] at the
-//                         first walked layer, else r_prev W with W = (A/c)^s (or
-//                         the clipped power) taken while streaming the fp32
-//                         score cache; one workgroup per (sequence, pair of
+//  walk_strip_kernel      step 5 on the query row only, for the score entries
+//                         the step leaves unchanged (rows and columns before
+//                         the open block): r_prev W with W = (A/c)^s (or the
+//                         clipped power) taken while streaming the fp32 score
+//                         cache; one workgroup per (sequence, pair of
 //                         32-column strips), the pairs balanced so that every
 //                         workgroup reads about as many rows, 32 row groups
 //                         reduced in LDS in a fixed order; the rows above a
 //                         strip, which hold only its decode-filled columns,
 //                         are shared by every thread of the workgroup
-//  walk_row_norm_kernel   divides the row by its largest magnitude (the
-//                         one-call step does this in select_decode_norm_kernel
-//                         before selecting, step 6)
+//  decode_sketch_walk_kernel  the one-call step's launch of both: the walk
+//                         workgroups and the sketch workgroups of a layer
+//                         side by side (they touch disjoint state)
+//  walk_row_norm_kernel   adds the open block's row and column terms to the
+//                         walk row and divides it by its largest magnitude
+//                         (the one-call step does this in
+//                         select_decode_norm_kernel before selecting, step 6)
 #include "select_row.h"
 #include "sw_common.h"
 #include "sw_internal.h"
@@ -59,9 +64,9 @@ __global__ __launch_bounds__(256) void decode_init_kernel(char* __restrict__ sta
   const DecodeLayout L = decode_layout(batch, d, r, b_max);
   const int m = blockIdx.x;              // row of the score cache
   const int b = (n + B - 1) / B;
-  float* Arow = reinterpret_cast<float*>(state + L.a) + ((long long)seq * b_max + m) * L.lda;
+  float* As = reinterpret_cast<float*>(state + L.a) + (long long)seq * b_max * L.lda;
   for (int j = threadIdx.x; j < L.lda; j += 256)
-    Arow[j] = (m < b && j < b) ? (float)A[(long long)m * b + j] : 0.0f;
+    As[cache_at(b_max, m, j)] = (m < b && j < b) ? (float)A[(long long)m * b + j] : 0.0f;
   if (m < b) {
     double* qs = reinterpret_cast<double*>(state + L.qs) + ((long long)seq * b_max + m) * r;
     double* ks = reinterpret_cast<double*>(state + L.ks) + ((long long)seq * b_max + m) * r;
@@ -139,25 +144,33 @@ constexpr int kScoreChunk = 64;
 //     exchanges).
 // APPEND (the one-call step): chunk 0 also writes k_new and v_new into the
 // caches Kc, Vc [batch][h_kv][T_max][d] at pos (Alg. 2 step 1).
+// LDS of one sketch workgroup (doubles): per head group partial sums of the
+// token's query and key, then six vectors of 256.
+template <typename T>
+constexpr int sketch_lds_doubles() {
+  return 2 * 256 * (16 / (int)sizeof(T)) + 6 * 256;
+}
+
 template <typename T, bool APPEND>
-__global__ __launch_bounds__(256) void decode_sketch_kernel(const T* __restrict__ q_new,
-                                                            const T* __restrict__ k_new, int h_q,
-                                                            int h_kv, int d, int B,
-                                                            const int32_t* __restrict__ pos,
-                                                            const int8_t* __restrict__ signs,
-                                                            const int32_t* __restrict__ cols, int r,
-                                                            int batch, int b_max,
-                                                            char* __restrict__ state,
-                                                            const T* __restrict__ v_new,
-                                                            T* __restrict__ Kc, T* __restrict__ Vc,
-                                                            int T_max) {
+__device__ __forceinline__ void decode_sketch_body(const T* __restrict__ q_new,
+                                                   const T* __restrict__ k_new, int h_q, int h_kv,
+                                                   int d, int B, const int32_t* __restrict__ pos,
+                                                   const int8_t* __restrict__ signs,
+                                                   const int32_t* __restrict__ cols, int r,
+                                                   int batch, int b_max, char* __restrict__ state,
+                                                   const T* __restrict__ v_new, T* __restrict__ Kc,
+                                                   T* __restrict__ Vc, int T_max, int bi, int chunk,
+                                                   double* lds) {
   constexpr int V = 16 / (int)sizeof(T);             // elements per 16-byte load
-  __shared__ double pq[256 * V], pk[256 * V];
-  __shared__ double xq[256], xb[256], xk[256];
-  __shared__ double sqt[256], sqb[256], skb[256];
+  double* pq = lds;
+  double* pk = pq + 256 * V;
+  double* xq = pk + 256 * V;
+  double* xb = xq + 256;
+  double* xk = xb + 256;
+  double* sqt = xk + 256;
+  double* sqb = sqt + 256;
+  double* skb = sqb + 256;
   const DecodeLayout L = decode_layout(batch, d, r, b_max);
-  const int bi = blockIdx.x;
-  const int chunk = blockIdx.y;
   const int t = threadIdx.x;
   // the new token's query/key chunks do not depend on the position: their
   // loads go out first (clamped head indices: no condition; extra ones unused)
@@ -312,10 +325,32 @@ __global__ __launch_bounds__(256) void decode_sketch_kernel(const T* __restrict_
   accr += __shfl_xor(accr, 2);
   accc += __shfl_xor(accc, 2);
   float* A = reinterpret_cast<float*>(state + L.a) + (long long)bi * b_max * L.lda;
+  float* rowc = reinterpret_cast<float*>(state + L.rowc) + (long long)bi * b_max;
+  float* colc = reinterpret_cast<float*>(state + L.colc) + (long long)bi * b_max;
   if (q4 == 0 && j <= bc) {
-    if (j < bc) A[(long long)bc * L.lda + j] = (float)(accr * rs);
-    A[(long long)j * L.lda + bc] = (float)(accc * rs);
+    const float vr = (float)(accr * rs), vc = (float)(accc * rs);
+    if (j < bc) A[cache_at(b_max, bc, j)] = vr;
+    A[cache_at(b_max, j, bc)] = vc;
+    rowc[j] = j < bc ? vr : vc;          // the diagonal entry comes from the column
+    colc[j] = vc;
   }
+}
+
+template <typename T, bool APPEND>
+__global__ __launch_bounds__(256) void decode_sketch_kernel(const T* __restrict__ q_new,
+                                                            const T* __restrict__ k_new, int h_q,
+                                                            int h_kv, int d, int B,
+                                                            const int32_t* __restrict__ pos,
+                                                            const int8_t* __restrict__ signs,
+                                                            const int32_t* __restrict__ cols, int r,
+                                                            int batch, int b_max,
+                                                            char* __restrict__ state,
+                                                            const T* __restrict__ v_new,
+                                                            T* __restrict__ Kc, T* __restrict__ Vc,
+                                                            int T_max) {
+  __shared__ double lds[sketch_lds_doubles<T>()];
+  decode_sketch_body<T, APPEND>(q_new, k_new, h_q, h_kv, d, B, pos, signs, cols, r, batch, b_max,
+                                state, v_new, Kc, Vc, T_max, blockIdx.x, blockIdx.y, lds);
 }
 
 // ---------------------------------------------------------------------------
@@ -350,45 +385,57 @@ __device__ __forceinline__ uint4 load_quad(__amdgpu_buffer_rsrc_t ra, int off) {
   return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(ra, off, 0, 0));
 }
 
-// One workgroup per (sequence, strip pair): strips k and S-1-k of 32 columns
-// (S = ceil(lda / 32)). Strip x's causal part is the rows m = 32 x .. b_cur
-// (every column of the strip can be non-zero there), so a pair holds about
-// b_cur rows in all. Its row groups are shared between the two strips in
-// proportion to their row counts; thread (row group g, column quad q) takes
-// every n-th row of its strip (n = the strip's group count) with 16-byte
-// loads of 4 columns, a row of a strip being one 128-byte piece. The columns
-// decode filled (col0 .. b_cur) are non-zero in the rows above the strip as
-// well (m < 32 x): those rows hold nothing else in the strip, so every thread
-// of the workgroup takes a share of them, for those columns only.
-// r_out[j] = (sum over the causal rows: per group ascending, then over the
+// The walk row splits into the part the step's sketch does not change and the
+// open block's row and column, which it rewrites (Alg. 2 step 4):
+//   r[j] = sum_{m != b_cur} r_prev[m] W[m][j]                 (j < b_cur)
+//          + r_prev[b_cur] W[b_cur][j]
+//   r[b_cur] = sum_{m <= b_cur} r_prev[m] W[m][b_cur]
+// walk_old_body computes the first sum from the score cache as the previous
+// steps left it (it reads no entry of row or column b_cur, so it may run
+// while the sketch of the same step writes them); walk_finish adds the rest.
+//
+// walk_old_body: one workgroup per (sequence, strip pair): strips k and
+// S-1-k of 32 columns (S = lda / 32; the cache stores a strip's rows
+// contiguously, 128 bytes each, so a strip is read as one contiguous range).
+// Strip x's rows m = 32 x .. b_cur - 1 hold its causal entries, so a pair
+// holds about b_cur rows in all. Its row groups are shared between the two
+// strips in proportion to their row counts; thread (row group g, column quad
+// q) takes every n-th row of its strip (n = the strip's group count) with
+// 16-byte loads of 4 columns. The columns decode filled before the open
+// block (col0 .. b_cur - 1) are non-zero in the rows above the strip as well
+// (m < 32 x): those rows hold nothing else in the strip, so every thread of
+// the workgroup takes a share of them, for those columns only.
+// r_out[j] = (sum over the strip's rows: per group ascending, then over the
 // strip's groups in blocks of 8, then over the blocks) + (sum over the rows
 // above: per thread ascending, then over the threads in blocks of 16, then
-// over the blocks) of r_prev[m] W[m][j]. Entries the score cache holds as
-// zero (above the diagonal outside the decode-filled columns, past b_cur)
-// give zero terms; quads that are wholly zero are not loaded. At the first
-// walked layer (r_prev NULL) the row of W itself, r_out[j] = W[b_cur][j].
-// Entries past b_cur are 0.
+// over the blocks) of r_prev[m] W[m][j] for j < b_cur. Entries the cache
+// holds as zero (above the diagonal outside the decode-filled columns) give
+// zero terms; quads that are wholly zero are not loaded.
+constexpr int kWalkSmem = kStripGroups * kStripCols > SW_MAX_BLOCKS ? kStripGroups * kStripCols
+                                                                    : SW_MAX_BLOCKS;
+constexpr int kWalkBlk = kStripGroups / 8;
+// LDS of one walk workgroup (doubles): the staged previous row, reused for the
+// row groups' sums; the block sums; the rows-above sums per thread, per block
+// of 16 threads and per column
+constexpr int kWalkLdsDoubles =
+    kWalkSmem + 2 * kWalkBlk * kStripCols + kStripThreads * 4 + (kStripThreads / 16) * 4 +
+    2 * kStripCols;
+
 template <bool S8, bool RELU>
-__global__ __launch_bounds__(kStripThreads) void walk_strip_kernel(const char* __restrict__ state,
-                                                                   int batch, int d, int r,
-                                                                   int b_max, int B,
-                                                                   const int32_t* __restrict__ pos,
-                                                                   int s_exp,
-                                                                   const double* __restrict__ r_prev,
-                                                                   double* __restrict__ r_out) {
-  // the walk row of the previous layer during the row loops, then the row
-  // groups' sums (both fit: b_max <= 4096 <= kStripGroups * kStripCols * 4)
-  constexpr int kSmem = kStripGroups * kStripCols > SW_MAX_BLOCKS ? kStripGroups * kStripCols
-                                                                  : SW_MAX_BLOCKS;
-  __shared__ double smem[kSmem];
-  __shared__ double red2[2][kStripGroups / 8][kStripCols];
-  __shared__ double xr[kStripThreads][4];
-  __shared__ double xred[kStripThreads / 16][4];
-  __shared__ double xsum[2][kStripCols];
+__device__ __forceinline__ void walk_old_body(const char* __restrict__ state, int batch, int d,
+                                              int r, int b_max, int B,
+                                              const int32_t* __restrict__ pos, int s_exp,
+                                              const double* __restrict__ r_prev,
+                                              double* __restrict__ r_out, int bi, int k,
+                                              double* lds) {
+  double* smem = lds;
+  double (*red2)[kWalkBlk][kStripCols] =
+      reinterpret_cast<double (*)[kWalkBlk][kStripCols]>(smem + kWalkSmem);
+  double (*xr)[4] = reinterpret_cast<double (*)[4]>(smem + kWalkSmem + 2 * kWalkBlk * kStripCols);
+  double (*xred)[4] = xr + kStripThreads;
+  double (*xsum)[kStripCols] = reinterpret_cast<double (*)[kStripCols]>(xred + kStripThreads / 16);
   const DecodeLayout L = decode_layout(batch, d, r, b_max);
   const int lda = L.lda;
-  const int bi = blockIdx.x;
-  const int k = blockIdx.y;
   const int t = threadIdx.x;
   // the loads that do not need the position go out with it: the scale, the
   // first decode-filled column and the whole previous walk row (clamped
@@ -397,7 +444,7 @@ __global__ __launch_bounds__(kStripThreads) void walk_strip_kernel(const char* _
   const double c0 = reinterpret_cast<const double*>(state + L.scale)[bi];
   const int col0 = reinterpret_cast<const int32_t*>(state + L.col0)[bi];
   constexpr int kStage = (SW_MAX_BLOCKS + kStripThreads - 1) / kStripThreads;
-  if (r_prev != nullptr) {
+  {
     double rs[kStage];
 #pragma unroll
     for (int i = 0; i < kStage; ++i)
@@ -408,18 +455,17 @@ __global__ __launch_bounds__(kStripThreads) void walk_strip_kernel(const char* _
   }
   const int bc = p / B;
   if (p < 0 || bc >= b_max) return;
-  const int S = (lda + kStripCols - 1) / kStripCols;
+  const int S = lda / kStripCols;
   const int sa = k, sb = S - 1 - k;                 // sb == sa: a single strip
   const double inv_c = 1.0 / (c0 > 0.0 ? c0 : 1.0);
   const float* A = reinterpret_cast<const float*>(state + L.a) + (long long)bi * b_max * lda;
   const int q = t % kStripQuads, g = t / kStripQuads;
-  const int na = (sa * kStripCols <= bc) ? bc - sa * kStripCols + 1 : 0;
-  const int nbr = (sb != sa && sb * kStripCols <= bc) ? bc - sb * kStripCols + 1 : 0;
+  const int na = (sa * kStripCols < bc) ? bc - sa * kStripCols : 0;
+  const int nbr = (sb != sa && sb * kStripCols < bc) ? bc - sb * kStripCols : 0;
   const int total = na + nbr;
   // row groups of strip a: about kStripGroups * na / total (each strip with
   // rows gets at least one)
-  int ga = (nbr == 0) ? kStripGroups
-                      : (na == 0 ? 0 : (int)(((long long)kStripGroups * na + total / 2) / total));
+  int ga = (nbr == 0) ? kStripGroups : (na == 0 ? 0 : (kStripGroups * na + total / 2) / total);
   if (na > 0 && nbr > 0) ga = min(max(ga, 1), kStripGroups - 1);
   const bool in_a = g < ga;
   const int x = in_a ? sa : sb;
@@ -428,23 +474,17 @@ __global__ __launch_bounds__(kStripThreads) void walk_strip_kernel(const char* _
   const int m0 = x * kStripCols;
   const int nrows = in_a ? na : nbr;
   const int j = x * kStripCols + 4 * q;             // this thread's 4 columns
-  const bool okj = j <= bc;                          // the quad holds a block
+  const bool okj = j < bc;                          // the quad holds an old column
+  const int ebc = bc - j;                           // element of column b_cur (if 0..3)
   // the sequence's score cache as a buffer: 32-bit offsets, and a load whose
   // quad holds nothing is sent past the end (it reads zeros)
   const int bytes = b_max * lda * 4;
   const __amdgpu_buffer_rsrc_t ra =
       __builtin_amdgcn_make_buffer_rsrc((void*)A, (short)0, bytes, kStripBufWord3);
   double acc[4] = {0.0, 0.0, 0.0, 0.0};
-  if (r_prev == nullptr) {
-    if (gi == 0 && nrows > 0 && okj) {
-      const float4 a = *reinterpret_cast<const float4*>(A + (long long)bc * lda + j);
-      const float av[4] = {a.x, a.y, a.z, a.w};
-#pragma unroll
-      for (int e = 0; e < 4; ++e) acc[e] = walk_weight<S8, RELU>(av[e], inv_c, s_exp);
-    }
-  } else {
-    __syncthreads();                     // the staged row is visible
-    const double* rp = smem;
+  __syncthreads();                       // the staged row is visible
+  const double* rp = smem;
+  {
     constexpr int NR = S8 ? SW_STRIP_ROWS : SW_STRIP_ROWS / 2;   // the general power needs more registers
     for (int i0 = gi; i0 < nrows; i0 += NR * ng) {
       // every load of the pass is issued before any is used
@@ -453,7 +493,7 @@ __global__ __launch_bounds__(kStripThreads) void walk_strip_kernel(const char* _
       for (int v = 0; v < NR; ++v) {
         const int i = i0 + v * ng;
         const bool ok = i < nrows && okj;
-        a[v] = load_quad(ra, ok ? ((m0 + i) * lda + j) * 4 : bytes);
+        a[v] = load_quad(ra, ok ? cache_at(b_max, m0 + i, j) * 4 : bytes);
       }
 #pragma unroll
       for (int v = 0; v < NR; ++v) {
@@ -461,64 +501,62 @@ __global__ __launch_bounds__(kStripThreads) void walk_strip_kernel(const char* _
         const float av[4] = {__uint_as_float(a[v].x), __uint_as_float(a[v].y),
                              __uint_as_float(a[v].z), __uint_as_float(a[v].w)};
 #pragma unroll
-        for (int e = 0; e < 4; ++e) acc[e] += rv * walk_weight<S8, RELU>(av[e], inv_c, s_exp);
+        for (int e = 0; e < 4; ++e)
+          if (e != ebc) acc[e] += rv * walk_weight<S8, RELU>(av[e], inv_c, s_exp);
       }
     }
   }
-  // the decode-filled columns of each strip over the rows above it
-  // (rows 0 .. 32 x - 1), one quad at a time, every thread a share of rows
+  // the decode-filled columns before b_cur of each strip over the rows above
+  // it (rows 0 .. 32 x - 1), one quad at a time, every thread a share of rows
   if (t < 2 * kStripCols) xsum[t / kStripCols][t % kStripCols] = 0.0;
   __syncthreads();
-  if (r_prev != nullptr) {
-    const double* rp = smem;
 #pragma unroll 1
-    for (int which = 0; which < 2; ++which) {
-      const int xs = which ? sb : sa;
-      if (which == 1 && sb == sa) break;
-      const int xj0 = xs * kStripCols;
-      if (xj0 > bc) continue;
-      const int qlo = max(col0 - xj0, 0) / 4, qhi = min(bc - xj0, kStripCols - 1) / 4;
-      if (xj0 + kStripCols - 1 < col0 || xj0 == 0) continue;
+  for (int which = 0; which < 2; ++which) {
+    const int xs = which ? sb : sa;
+    if (which == 1 && sb == sa) break;
+    const int xj0 = xs * kStripCols;
+    const int jlo = max(col0, xj0), jhi = min(bc - 1, xj0 + kStripCols - 1);
+    if (xj0 == 0 || jlo > jhi) continue;
 #pragma unroll 1
-      for (int qd = qlo; qd <= qhi; ++qd) {
-        const int jd = xj0 + 4 * qd;
-        double xa[4] = {0.0, 0.0, 0.0, 0.0};
-        for (int m1 = t; m1 < xj0; m1 += 8 * kStripThreads) {
-          uint4 a[8];
+    for (int qd = (jlo - xj0) / 4; qd <= (jhi - xj0) / 4; ++qd) {
+      const int jd = xj0 + 4 * qd;
+      double xa[4] = {0.0, 0.0, 0.0, 0.0};
+      for (int m1 = t; m1 < xj0; m1 += 8 * kStripThreads) {
+        uint4 a[8];
 #pragma unroll
-          for (int v = 0; v < 8; ++v) {
-            const int m = m1 + v * kStripThreads;
-            a[v] = load_quad(ra, m < xj0 ? (m * lda + jd) * 4 : bytes);
-          }
-#pragma unroll
-          for (int v = 0; v < 8; ++v) {
-            const double rv = rp[min(m1 + v * kStripThreads, xj0 - 1)];
-            const float av[4] = {__uint_as_float(a[v].x), __uint_as_float(a[v].y),
-                                 __uint_as_float(a[v].z), __uint_as_float(a[v].w)};
-#pragma unroll
-            for (int e = 0; e < 4; ++e) xa[e] += rv * walk_weight<S8, RELU>(av[e], inv_c, s_exp);
-          }
+        for (int v = 0; v < 8; ++v) {
+          const int m = m1 + v * kStripThreads;
+          a[v] = load_quad(ra, m < xj0 ? cache_at(b_max, m, jd) * 4 : bytes);
         }
-        // fixed-order reduction over the threads: blocks of 16, then the blocks
 #pragma unroll
-        for (int e = 0; e < 4; ++e) xr[t][e] = xa[e];
-        __syncthreads();
-        if (t < (kStripThreads / 16) * 4) {
-          const int bk = t / 4, e = t % 4;
-          double v = 0.0;
+        for (int v = 0; v < 8; ++v) {
+          const double rv = rp[min(m1 + v * kStripThreads, xj0 - 1)];
+          const float av[4] = {__uint_as_float(a[v].x), __uint_as_float(a[v].y),
+                               __uint_as_float(a[v].z), __uint_as_float(a[v].w)};
 #pragma unroll
-          for (int u = 0; u < 16; ++u) v += xr[bk * 16 + u][e];
-          xred[bk][e] = v;
+          for (int e = 0; e < 4; ++e)
+            if (jd + e != bc) xa[e] += rv * walk_weight<S8, RELU>(av[e], inv_c, s_exp);
         }
-        __syncthreads();
-        if (t < 4) {
-          double v = 0.0;
-#pragma unroll
-          for (int u = 0; u < kStripThreads / 16; ++u) v += xred[u][t];
-          xsum[which][4 * qd + t] = v;
-        }
-        __syncthreads();
       }
+      // fixed-order reduction over the threads: blocks of 16, then the blocks
+#pragma unroll
+      for (int e = 0; e < 4; ++e) xr[t][e] = xa[e];
+      __syncthreads();
+      if (t < (kStripThreads / 16) * 4) {
+        const int bk = t / 4, e = t % 4;
+        double v = 0.0;
+#pragma unroll
+        for (int u = 0; u < 16; ++u) v += xr[bk * 16 + u][e];
+        xred[bk][e] = v;
+      }
+      __syncthreads();
+      if (t < 4) {
+        double v = 0.0;
+#pragma unroll
+        for (int u = 0; u < kStripThreads / 16; ++u) v += xred[u][t];
+        xsum[which][4 * qd + t] = v;
+      }
+      __syncthreads();
     }
   }
   __syncthreads();
@@ -528,9 +566,9 @@ __global__ __launch_bounds__(kStripThreads) void walk_strip_kernel(const char* _
   __syncthreads();
   // fixed-order reduction over a strip's groups: sums of 8 consecutive groups
   // (one per thread: strip, block of 8 groups, column), then of the blocks
-  constexpr int kBlk = kStripGroups / 8;
   {
-    const int which = t / (kBlk * kStripCols), bk = (t / kStripCols) % kBlk, c = t % kStripCols;
+    const int which = t / (kWalkBlk * kStripCols), bk = (t / kStripCols) % kWalkBlk,
+              c = t % kStripCols;
     const int g0 = which ? ga : 0, g1 = which ? kStripGroups : ga;
     double vals[8];
 #pragma unroll
@@ -545,21 +583,125 @@ __global__ __launch_bounds__(kStripThreads) void walk_strip_kernel(const char* _
     const int which = t / kStripCols, c = t % kStripCols;
     if (which == 0 || sb != sa) {
       const int xs = which ? sb : sa;
-      double vals[kBlk];
+      double vals[kWalkBlk];
 #pragma unroll
-      for (int u = 0; u < kBlk; ++u) vals[u] = red2[which][u][c];
+      for (int u = 0; u < kWalkBlk; ++u) vals[u] = red2[which][u][c];
       double v = 0.0;
 #pragma unroll
-      for (int u = 0; u < kBlk; ++u) v += vals[u];
+      for (int u = 0; u < kWalkBlk; ++u) v += vals[u];
       const int jj = xs * kStripCols + c;
-      if (r_prev != nullptr && jj >= col0 && xs * kStripCols > 0) v += xsum[which][c];
-      if (jj < b_max) r_out[(long long)bi * b_max + jj] = (jj <= bc) ? v : 0.0;
+      if (jj >= col0 && xs * kStripCols > 0) v += xsum[which][c];
+      if (jj < bc) r_out[(long long)bi * b_max + jj] = v;
     }
   }
 }
 
-__global__ __launch_bounds__(256) void walk_row_norm_kernel(int b_max, int B,
-                                                            const int32_t* __restrict__ pos,
+// Per-layer form: the unchanged part of the walk row into r_out[j], j < b_cur
+// (walk_row_norm_kernel completes it).
+template <bool S8, bool RELU>
+__global__ __launch_bounds__(kStripThreads) void walk_strip_kernel(const char* __restrict__ state,
+                                                                   int batch, int d, int r,
+                                                                   int b_max, int B,
+                                                                   const int32_t* __restrict__ pos,
+                                                                   int s_exp,
+                                                                   const double* __restrict__ r_prev,
+                                                                   double* __restrict__ r_out) {
+  __shared__ double lds[kWalkLdsDoubles];
+  walk_old_body<S8, RELU>(state, batch, d, r, b_max, B, pos, s_exp, r_prev, r_out, blockIdx.x,
+                          blockIdx.y, lds);
+}
+
+// The one-call step: the workgroups with blockIdx.y < pairs compute the
+// unchanged part of this layer's walk row (none at the first walked layer),
+// the others run the incremental sketch (with the KV append). The two read
+// and write disjoint parts of the state, so they run side by side.
+template <typename T, bool S8, bool RELU>
+__global__ __launch_bounds__(256) void decode_sketch_walk_kernel(
+    const T* __restrict__ q_new, const T* __restrict__ k_new, int h_q, int h_kv, int d, int B,
+    const int32_t* __restrict__ pos, const int8_t* __restrict__ signs,
+    const int32_t* __restrict__ cols, int r, int batch, int b_max, char* __restrict__ state,
+    const T* __restrict__ v_new, T* __restrict__ Kc, T* __restrict__ Vc, int T_max, int pairs,
+    int s_exp, const double* __restrict__ r_prev, double* __restrict__ rows) {
+  static_assert(kStripThreads == 256, "both roles run 256 threads");
+  constexpr int kLds = sketch_lds_doubles<T>() > kWalkLdsDoubles ? sketch_lds_doubles<T>()
+                                                                 : kWalkLdsDoubles;
+  __shared__ double lds[kLds];
+  if ((int)blockIdx.y < pairs)
+    walk_old_body<S8, RELU>(state, batch, d, r, b_max, B, pos, s_exp, r_prev, rows, blockIdx.x,
+                            blockIdx.y, lds);
+  else
+    decode_sketch_body<T, true>(q_new, k_new, h_q, h_kv, d, B, pos, signs, cols, r, batch, b_max,
+                                state, v_new, Kc, Vc, T_max, blockIdx.x, blockIdx.y - pairs, lds);
+}
+
+// walk_finish: thread t's values v[e] of the finished (unnormalised) walk row
+// for blocks j = t*E + e <= b_cur (E = ceil((b_cur + 1) / 256)), from the
+// unchanged part in old[j] (j < b_cur; not read when r_prev is NULL) and the
+// open block's row and column of the score cache. At the first walked layer
+// (r_prev NULL) the row is W[b_cur][j] itself. The column sum runs per
+// thread over m = t, t + 256, ... ascending, then over the lanes of a
+// wavefront by exchanges and over the four wavefronts in order.
+template <bool S8, bool RELU, int MAXE>
+__device__ __forceinline__ void walk_finish(const char* __restrict__ state, int batch, int d, int r,
+                                            int b_max, int bi, int bc, int s_exp,
+                                            const double* __restrict__ r_prev,
+                                            const double* __restrict__ old, double (&v)[MAXE],
+                                            double* tmp) {
+  const DecodeLayout L = decode_layout(batch, d, r, b_max);
+  const int t = threadIdx.x;
+  const int avail = bc + 1;
+  const int E = (avail + 255) / 256;
+  const double c0 = reinterpret_cast<const double*>(state + L.scale)[bi];
+  const double inv_c = 1.0 / (c0 > 0.0 ? c0 : 1.0);
+  const float* rowc = reinterpret_cast<const float*>(state + L.rowc) + (long long)bi * b_max;
+  const float* colc = reinterpret_cast<const float*>(state + L.colc) + (long long)bi * b_max;
+  // every load goes out before any value is used (indices clamped into range)
+  float wrow[MAXE];
+#pragma unroll
+  for (int e = 0; e < MAXE; ++e) wrow[e] = rowc[min(t * E + e, bc)];
+  if (r_prev == nullptr) {
+#pragma unroll
+    for (int e = 0; e < MAXE; ++e) v[e] = walk_weight<S8, RELU>(wrow[e], inv_c, s_exp);
+    return;
+  }
+  const double* rp = r_prev + (long long)bi * b_max;
+  double ov[MAXE];
+#pragma unroll
+  for (int e = 0; e < MAXE; ++e) ov[e] = old[min(t * E + e, max(bc - 1, 0))];
+  float wcol[MAXE];
+  double rcol[MAXE];
+#pragma unroll
+  for (int e = 0; e < MAXE; ++e) {
+    const int m = min(t + 256 * e, bc);
+    wcol[e] = colc[m];
+    rcol[e] = rp[m];
+  }
+  const double rb = rp[bc];
+  double cs = 0.0;
+#pragma unroll
+  for (int e = 0; e < MAXE; ++e)
+    if (t + 256 * e <= bc) cs += rcol[e] * walk_weight<S8, RELU>(wcol[e], inv_c, s_exp);
+  for (int off = 1; off < 64; off <<= 1) cs += __shfl_xor(cs, off);
+  if ((t & 63) == 0) tmp[t >> 6] = cs;
+  __syncthreads();
+  cs = ((tmp[0] + tmp[1]) + tmp[2]) + tmp[3];
+  __syncthreads();
+#pragma unroll
+  for (int e = 0; e < MAXE; ++e) {
+    const int j = t * E + e;
+    v[e] = (j < bc) ? ov[e] + rb * walk_weight<S8, RELU>(wrow[e], inv_c, s_exp) : cs;
+  }
+}
+
+// Per-layer form of the walk's completion: r_out[j] (j <= b_cur) finished
+// from its unchanged part and divided by its largest magnitude; entries past
+// b_cur are zeroed.
+template <bool S8, bool RELU, int MAXE>
+__global__ __launch_bounds__(256) void walk_row_norm_kernel(const char* __restrict__ state,
+                                                            int batch, int d, int r, int b_max,
+                                                            int B, const int32_t* __restrict__ pos,
+                                                            int s_exp,
+                                                            const double* __restrict__ r_prev,
                                                             double* __restrict__ r_out) {
   __shared__ double tmp[4];
   const int bi = blockIdx.x;
@@ -567,27 +709,39 @@ __global__ __launch_bounds__(256) void walk_row_norm_kernel(int b_max, int B,
   const int bc = p / B;
   if (p < 0 || bc >= b_max) return;
   double* out = r_out + (long long)bi * b_max;
+  const int t = threadIdx.x;
+  const int avail = bc + 1;
+  const int E = (avail + 255) / 256;
+  double v[MAXE];
+  walk_finish<S8, RELU, MAXE>(state, batch, d, r, b_max, bi, bc, s_exp, r_prev, out, v, tmp);
   double mx = 0.0;
-  for (int j = threadIdx.x; j <= bc; j += 256) mx = fmax(mx, fabs(out[j]));
+#pragma unroll
+  for (int e = 0; e < MAXE; ++e)
+    if (e < E && t * E + e < avail) mx = fmax(mx, fabs(v[e]));
   for (int off = 32; off > 0; off >>= 1) mx = fmax(mx, __shfl_xor(mx, off));
-  if ((threadIdx.x & 63) == 0) tmp[threadIdx.x >> 6] = mx;
+  if ((t & 63) == 0) tmp[t >> 6] = mx;
   __syncthreads();
   mx = fmax(fmax(tmp[0], tmp[1]), fmax(tmp[2], tmp[3]));
   const double inv = mx > 0.0 ? 1.0 / mx : 1.0;
-  for (int j = threadIdx.x; j < b_max; j += 256) out[j] = (j <= bc) ? out[j] * inv : 0.0;
+#pragma unroll
+  for (int e = 0; e < MAXE; ++e) {
+    const int j = t * E + e;
+    if (e < E && j < avail) out[j] = v[e] * inv;
+  }
+  for (int j = avail + t; j < b_max; j += 256) out[j] = 0.0;
 }
 
-// The one-call step: the walk row of each sequence divided in place by its
-// largest magnitude over blocks 0..b_cur (entries past b_cur zeroed), then its
-// selection (Alg. 2 step 6, forced set {0, b_cur}) from the rescaled values
-// the threads still hold in registers.
-__global__ __launch_bounds__(256) void select_decode_norm_kernel(double* __restrict__ rows,
-                                                                 int b_max, int B,
-                                                                 const int32_t* __restrict__ pos,
-                                                                 int k, int pct, uint32_t flags,
-                                                                 int32_t* __restrict__ idx,
-                                                                 int32_t* __restrict__ cnt,
-                                                                 int kmax) {
+// The one-call step: the walk row of each sequence finished from its
+// unchanged part in rows, divided in place by its largest magnitude over
+// blocks 0..b_cur (entries past b_cur zeroed), then its selection (Alg. 2
+// step 6, forced set {0, b_cur}) from the rescaled values the threads still
+// hold in registers.
+template <bool S8, bool RELU, int MAXE>
+__global__ __launch_bounds__(256) void select_decode_norm_kernel(
+    const char* __restrict__ state, int batch, int d, int r, int b_max, int B,
+    const int32_t* __restrict__ pos, int s_exp, const double* __restrict__ r_prev,
+    double* __restrict__ rows, int k, int pct, uint32_t flags, int32_t* __restrict__ idx,
+    int32_t* __restrict__ cnt, int kmax) {
   __shared__ double tmp[4];
   const int bi = blockIdx.x;
   const int p = pos[bi];
@@ -597,11 +751,11 @@ __global__ __launch_bounds__(256) void select_decode_norm_kernel(double* __restr
   const int avail = bc + 1;
   const int E = (avail + 255) / 256;
   const int t = threadIdx.x;
-  double v[kMaxPerThread];
-  load_row_vals(row, avail, v);
+  double v[MAXE];
+  walk_finish<S8, RELU, MAXE>(state, batch, d, r, b_max, bi, bc, s_exp, r_prev, row, v, tmp);
   double mx = 0.0;
 #pragma unroll
-  for (int e = 0; e < kMaxPerThread; ++e)
+  for (int e = 0; e < MAXE; ++e)
     if (e < E && t * E + e < avail) mx = fmax(mx, fabs(v[e]));
   for (int off = 32; off > 0; off >>= 1) mx = fmax(mx, __shfl_xor(mx, off));
   if ((t & 63) == 0) tmp[t >> 6] = mx;
@@ -609,7 +763,7 @@ __global__ __launch_bounds__(256) void select_decode_norm_kernel(double* __restr
   mx = fmax(fmax(tmp[0], tmp[1]), fmax(tmp[2], tmp[3]));
   const double inv = mx > 0.0 ? 1.0 / mx : 1.0;
 #pragma unroll
-  for (int e = 0; e < kMaxPerThread; ++e) {
+  for (int e = 0; e < MAXE; ++e) {
     const int j = t * E + e;
     if (e < E && j < avail) {
       v[e] = v[e] * inv;
@@ -619,7 +773,7 @@ __global__ __launch_bounds__(256) void select_decode_norm_kernel(double* __restr
   for (int j = avail + t; j < b_max; j += 256) row[j] = 0.0;
   const int first = (flags & SW_FORCE_FIRST) ? 0 : -1;
   const int last = (flags & SW_FORCE_LAST) ? bc : -1;
-  select_row_vals(v, avail, first, last, k, pct, idx + (long long)bi * kmax, cnt + bi, kmax);
+  select_row_vals<MAXE>(v, avail, first, last, k, pct, idx + (long long)bi * kmax, cnt + bi, kmax);
 }
 
 // ---------------------------------------------------------------------------
@@ -672,19 +826,8 @@ void launch_sketch_t(const void* q_new, const void* k_new, int batch, int h_q, i
                        static_cast<T*>(nullptr), T_max);
 }
 
-void launch_strips(const char* state, int batch, int d, int r, int b_max, int B, const int32_t* pos,
-                   int s_exp, bool relu, const double* r_prev, double* r_out, hipStream_t st) {
-  const int lda = (b_max + 3) & ~3;
-  const int S = (lda + kStripCols - 1) / kStripCols;
-  const dim3 grid((unsigned)batch, (unsigned)((S + 1) / 2)), blk(kStripThreads);
-#define SW_STRIP_LAUNCH(S8, RELU)                                                                \
-  hipLaunchKernelGGL((walk_strip_kernel<S8, RELU>), grid, blk, 0, st, state, batch, d, r, b_max, \
-                     B, pos, s_exp, r_prev, r_out)
-  if (s_exp == 8 && !relu) SW_STRIP_LAUNCH(true, false);
-  else if (s_exp == 8) SW_STRIP_LAUNCH(true, true);
-  else if (!relu) SW_STRIP_LAUNCH(false, false);
-  else SW_STRIP_LAUNCH(false, true);
-#undef SW_STRIP_LAUNCH
+int strip_pairs(int batch, int d, int r, int b_max) {
+  return (decode_layout(batch, d, r, b_max).lda / kStripCols + 1) / 2;
 }
 
 }  // namespace
@@ -705,20 +848,93 @@ hipError_t launch_decode_sketch(int dtype, const void* q_new, const void* k_new,
 hipError_t launch_decode_walk(const char* state, int batch, int d, int r, int b_max, int B,
                               const int32_t* pos, int s_exp, bool relu, const double* r_prev,
                               double* r_out, hipStream_t st) {
-  launch_strips(state, batch, d, r, b_max, B, pos, s_exp, relu, r_prev, r_out, st);
-  hipLaunchKernelGGL(walk_row_norm_kernel, dim3((unsigned)batch), dim3(256), 0, st, b_max, B, pos,
-                     r_out);
+  const dim3 grid((unsigned)batch, (unsigned)strip_pairs(batch, d, r, b_max));
+#define SW_NORM_LAUNCH(S8, RELU, E)                                                              \
+  hipLaunchKernelGGL((walk_row_norm_kernel<S8, RELU, E>), dim3((unsigned)batch), dim3(256), 0, st, \
+                     state, batch, d, r, b_max, B, pos, s_exp, r_prev, r_out)
+#define SW_WALK_LAUNCH(S8, RELU)                                                                   \
+  do {                                                                                            \
+    if (r_prev != nullptr)                                                                        \
+      hipLaunchKernelGGL((walk_strip_kernel<S8, RELU>), grid, dim3(kStripThreads), 0, st, state,  \
+                         batch, d, r, b_max, B, pos, s_exp, r_prev, r_out);                       \
+    switch (row_maxe(b_max)) {                                                                    \
+      case 2: SW_NORM_LAUNCH(S8, RELU, 2); break;                                                 \
+      case 4: SW_NORM_LAUNCH(S8, RELU, 4); break;                                                 \
+      case 8: SW_NORM_LAUNCH(S8, RELU, 8); break;                                                 \
+      default: SW_NORM_LAUNCH(S8, RELU, 16); break;                                               \
+    }                                                                                             \
+  } while (0)
+  if (s_exp == 8 && !relu) SW_WALK_LAUNCH(true, false);
+  else if (s_exp == 8) SW_WALK_LAUNCH(true, true);
+  else if (!relu) SW_WALK_LAUNCH(false, false);
+  else SW_WALK_LAUNCH(false, true);
+#undef SW_WALK_LAUNCH
+#undef SW_NORM_LAUNCH
   return hipGetLastError();
 }
 
-hipError_t launch_decode_walk_select(const char* state, int batch, int d, int r, int b_max, int B,
-                                     const int32_t* pos, int s_exp, bool relu,
-                                     const double* r_prev, double* rows, int k, int pct,
-                                     uint32_t flags, int32_t* idx, int32_t* cnt, int kmax,
-                                     hipStream_t st) {
-  launch_strips(state, batch, d, r, b_max, B, pos, s_exp, relu, r_prev, rows, st);
-  hipLaunchKernelGGL(select_decode_norm_kernel, dim3((unsigned)batch), dim3(256), 0, st, rows,
-                     b_max, B, pos, k, pct, flags, idx, cnt, kmax);
+namespace {
+
+template <typename T, bool S8, bool RELU>
+void launch_layer_t(const void* q_new, const void* k_new, const void* v_new, void* Kc, void* Vc,
+                    int T_max, int batch, int h_q, int h_kv, int d, int B, const int32_t* pos,
+                    const int8_t* signs, const int32_t* cols, int r, int b_max, char* state,
+                    int s_exp, const double* r_prev, double* rows, int k, int pct, uint32_t flags,
+                    int32_t* idx, int32_t* cnt, int kmax, hipStream_t st) {
+  const int pairs = r_prev != nullptr ? strip_pairs(batch, d, r, b_max) : 0;
+  const int chunks = (b_max + kScoreChunk - 1) / kScoreChunk;
+  hipLaunchKernelGGL((decode_sketch_walk_kernel<T, S8, RELU>),
+                     dim3((unsigned)batch, (unsigned)(pairs + chunks)), dim3(256), 0, st,
+                     reinterpret_cast<const T*>(q_new), reinterpret_cast<const T*>(k_new), h_q,
+                     h_kv, d, B, pos, signs, cols, r, batch, b_max, state,
+                     reinterpret_cast<const T*>(v_new), reinterpret_cast<T*>(Kc),
+                     reinterpret_cast<T*>(Vc), T_max, pairs, s_exp, r_prev, rows);
+#define SW_SEL_LAUNCH(E)                                                                        \
+  hipLaunchKernelGGL((select_decode_norm_kernel<S8, RELU, E>), dim3((unsigned)batch), dim3(256), 0, \
+                     st, state, batch, d, r, b_max, B, pos, s_exp, r_prev, rows, k, pct, flags,    \
+                     idx, cnt, kmax)
+  switch (row_maxe(b_max)) {
+    case 2: SW_SEL_LAUNCH(2); break;
+    case 4: SW_SEL_LAUNCH(4); break;
+    case 8: SW_SEL_LAUNCH(8); break;
+    default: SW_SEL_LAUNCH(16); break;
+  }
+#undef SW_SEL_LAUNCH
+}
+
+template <typename T>
+void launch_layer_w(bool relu, const void* q_new, const void* k_new, const void* v_new, void* Kc,
+                    void* Vc, int T_max, int batch, int h_q, int h_kv, int d, int B,
+                    const int32_t* pos, const int8_t* signs, const int32_t* cols, int r, int b_max,
+                    char* state, int s_exp, const double* r_prev, double* rows, int k, int pct,
+                    uint32_t flags, int32_t* idx, int32_t* cnt, int kmax, hipStream_t st) {
+#define SW_LAYER(S8, RELU)                                                                     \
+  launch_layer_t<T, S8, RELU>(q_new, k_new, v_new, Kc, Vc, T_max, batch, h_q, h_kv, d, B, pos, \
+                              signs, cols, r, b_max, state, s_exp, r_prev, rows, k, pct, flags, \
+                              idx, cnt, kmax, st)
+  if (s_exp == 8 && !relu) SW_LAYER(true, false);
+  else if (s_exp == 8) SW_LAYER(true, true);
+  else if (!relu) SW_LAYER(false, false);
+  else SW_LAYER(false, true);
+#undef SW_LAYER
+}
+
+}  // namespace
+
+hipError_t launch_decode_layer(int dtype, const void* q_new, const void* k_new, const void* v_new,
+                               void* Kc, void* Vc, int T_max, int batch, int h_q, int h_kv, int d,
+                               int B, const int32_t* pos, const int8_t* signs, const int32_t* cols,
+                               int r, int b_max, char* state, int s_exp, bool relu,
+                               const double* r_prev, double* rows, int k, int pct, uint32_t flags,
+                               int32_t* idx, int32_t* cnt, int kmax, hipStream_t st) {
+  if (dtype == SW_BF16)
+    launch_layer_w<uint16_t>(relu, q_new, k_new, v_new, Kc, Vc, T_max, batch, h_q, h_kv, d, B, pos,
+                             signs, cols, r, b_max, state, s_exp, r_prev, rows, k, pct, flags, idx,
+                             cnt, kmax, st);
+  else
+    launch_layer_w<float>(relu, q_new, k_new, v_new, Kc, Vc, T_max, batch, h_q, h_kv, d, B, pos,
+                          signs, cols, r, b_max, state, s_exp, r_prev, rows, k, pct, flags, idx,
+                          cnt, kmax, st);
   return hipGetLastError();
 }
 

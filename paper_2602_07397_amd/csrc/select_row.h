@@ -14,7 +14,6 @@
 
 namespace sw {
 
-constexpr int kMaxPerThread = SW_MAX_BLOCKS / 256;
 
 __device__ __forceinline__ int row_budget_dev(int avail, int nf, int k, int pct) {
   int t = (k > 0) ? k : (avail * pct + 99) / 100;
@@ -22,27 +21,40 @@ __device__ __forceinline__ int row_budget_dev(int avail, int nf, int k, int pct)
   return min(t, avail);
 }
 
+// Kernels over rows of at most 256 * MAXE blocks hold MAXE values per
+// thread (MAXE in {2, 4, 8, 16}); launchers pick the smallest that fits.
+inline int row_maxe(int max_avail) {
+  const int e = (max_avail + 255) / 256;
+  return e <= 2 ? 2 : e <= 4 ? 4 : e <= 8 ? 8 : 16;
+}
+
 // This thread's values of a row: v[e] = vals[t*E + e] for the blocks it owns
-// (E = ceil(avail / 256); entries e >= E are never used). The loads carry no
-// condition (the index is clamped into the row), so all of them are in
-// flight before the first value is used.
+// (E = ceil(avail / 256) <= MAXE; entries e >= E are never used). The loads
+// carry no condition (the index is clamped into the row), so all of them are
+// in flight before the first value is used.
+template <int MAXE>
 __device__ __forceinline__ void load_row_vals(const double* __restrict__ vals, int avail,
-                                              double (&v)[kMaxPerThread]) {
+                                              double (&v)[MAXE]) {
   const int t = threadIdx.x;
   const int E = (avail + 255) / 256;
 #pragma unroll
-  for (int e = 0; e < kMaxPerThread; ++e) v[e] = vals[min(t * E + e, avail - 1)];
+  for (int e = 0; e < MAXE; ++e) v[e] = vals[min(t * E + e, avail - 1)];
 }
 
 // Selects from the row held as per-thread values v (as load_row_vals lays
-// them out) with forced set {first, last} (-1 = none).
-__device__ __forceinline__ void select_row_vals(const double (&v)[kMaxPerThread], int avail,
-                                                int first, int last, int k, int pct,
+// them out) with forced set {first, last} (-1 = none). The radix passes
+// start at the first byte where the smallest and largest candidate keys
+// differ (the bytes before it put every candidate in one bin).
+template <int MAXE>
+__device__ __forceinline__ void select_row_vals(const double (&v)[MAXE], int avail, int first,
+                                                int last, int k, int pct,
                                                 int32_t* __restrict__ out,
                                                 int32_t* __restrict__ cnt, int kmax) {
+  static_assert(MAXE <= 32, "one mask bit per value");
   __shared__ int hist[256];
   __shared__ int scan_tmp[256];
   __shared__ int sh_digit, sh_need, sh_cnt;
+  __shared__ unsigned long long klo[4], khi[4];
   const int t = threadIdx.x;
   const int E = (avail + 255) / 256;
   const int nf = (first >= 0) + (last >= 0 && last != first);
@@ -50,10 +62,10 @@ __device__ __forceinline__ void select_row_vals(const double (&v)[kMaxPerThread]
   const int m = tau - nf;                 // ranked blocks to take
   const int nc = avail - nf;              // ranked candidates
 
-  unsigned long long key[kMaxPerThread];
+  unsigned long long key[MAXE];
   uint32_t candmask = 0, forcedmask = 0;
 #pragma unroll
-  for (int e = 0; e < kMaxPerThread; ++e) {
+  for (int e = 0; e < MAXE; ++e) {
     key[e] = 0ull;
     const int j = t * E + e;
     if (e < E && j < avail) {
@@ -74,12 +86,39 @@ __device__ __forceinline__ void select_row_vals(const double (&v)[kMaxPerThread]
   bool take_all_eq = false;
   const bool partial = (m > 0 && m < nc);
   if (partial) {
-    for (int pass = 0; pass < 8; ++pass) {
+    unsigned long long lo = ~0ull, hi = 0ull;
+#pragma unroll
+    for (int e = 0; e < MAXE; ++e)
+      if ((candmask >> e) & 1u) {
+        lo = key[e] < lo ? key[e] : lo;
+        hi = key[e] > hi ? key[e] : hi;
+      }
+    for (int off = 32; off > 0; off >>= 1) {
+      const unsigned long long ol = __shfl_xor(lo, off), oh = __shfl_xor(hi, off);
+      lo = ol < lo ? ol : lo;
+      hi = oh > hi ? oh : hi;
+    }
+    if ((t & 63) == 0) {
+      klo[t >> 6] = lo;
+      khi[t >> 6] = hi;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      lo = klo[w] < lo ? klo[w] : lo;
+      hi = khi[w] > hi ? khi[w] : hi;
+    }
+    const int same = (lo == hi) ? 8 : (__clzll((long long)(lo ^ hi)) >> 3);
+    if (same > 0) {
+      pmask = (same == 8) ? ~0ull : (~0ull << (64 - 8 * same));
+      prefix = lo & pmask;
+    }
+    for (int pass = same; pass < 8; ++pass) {
       const int shift = 56 - 8 * pass;
       hist[t] = 0;
       __syncthreads();
 #pragma unroll
-      for (int e = 0; e < kMaxPerThread; ++e)
+      for (int e = 0; e < MAXE; ++e)
         if ((candmask >> e) & 1u)
           if ((key[e] & pmask) == prefix) atomicAdd(&hist[(int)((key[e] >> shift) & 255ull)], 1);
       __syncthreads();
@@ -108,7 +147,7 @@ __device__ __forceinline__ void select_row_vals(const double (&v)[kMaxPerThread]
   int my_eq = 0;
   if (partial && !take_all_eq) {
 #pragma unroll
-    for (int e = 0; e < kMaxPerThread; ++e)
+    for (int e = 0; e < MAXE; ++e)
       if (((candmask >> e) & 1u) && (key[e] & pmask) == prefix) ++my_eq;
   }
   int dummy;
@@ -116,7 +155,7 @@ __device__ __forceinline__ void select_row_vals(const double (&v)[kMaxPerThread]
 
   uint32_t selmask = forcedmask;
 #pragma unroll
-  for (int e = 0; e < kMaxPerThread; ++e) {
+  for (int e = 0; e < MAXE; ++e) {
     if ((candmask >> e) & 1u) {
       bool take;
       const unsigned long long kk = key[e] & pmask;
@@ -132,19 +171,20 @@ __device__ __forceinline__ void select_row_vals(const double (&v)[kMaxPerThread]
   int total_sel;
   int pos = block_exclusive_scan_256(mine, scan_tmp, &total_sel);
 #pragma unroll
-  for (int e = 0; e < kMaxPerThread; ++e)
+  for (int e = 0; e < MAXE; ++e)
     if ((selmask >> e) & 1u) out[pos++] = t * E + e;
   for (int q = tau + t; q < kmax; q += 256) out[q] = -1;
   if (t == 0) *cnt = tau;
 }
 
 // Selects from vals[0..avail) with forced set {first, last} (-1 = none).
+template <int MAXE>
 __device__ __forceinline__ void select_row_dev(const double* __restrict__ vals, int avail, int first,
                                                int last, int k, int pct, int32_t* __restrict__ out,
                                                int32_t* __restrict__ cnt, int kmax) {
-  double v[kMaxPerThread];
-  load_row_vals(vals, avail, v);
-  select_row_vals(v, avail, first, last, k, pct, out, cnt, kmax);
+  double v[MAXE];
+  load_row_vals<MAXE>(vals, avail, v);
+  select_row_vals<MAXE>(v, avail, first, last, k, pct, out, cnt, kmax);
 }
 
 }  // namespace sw

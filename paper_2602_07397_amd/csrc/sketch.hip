@@ -15,6 +15,9 @@
 #include "sw_common.h"
 #include "sw_internal.h"
 
+#define SW_STR2(x) #x
+#define SW_STR(x) SW_STR2(x)
+
 namespace sw {
 
 typedef double f64x4 __attribute__((ext_vector_type(4)));
@@ -24,6 +27,9 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 #define SW_POOL_THREADS 512
 #endif
 constexpr int kPoolThreads = SW_POOL_THREADS;
+#ifndef SW_POOL_UNROLL
+#define SW_POOL_UNROLL 8
+#endif
 
 template <typename T>
 __global__ __launch_bounds__(kPoolThreads) void pool_sketch_kernel(
@@ -76,7 +82,7 @@ __global__ __launch_bounds__(kPoolThreads) void pool_sketch_kernel(
   const int dh = slots / cnt, dt = slots % cnt;
   {
     int h = slot / cnt, tok = slot % cnt;
-#pragma unroll 8
+_Pragma(SW_STR(unroll SW_POOL_UNROLL))
     for (int it = slot; it < nq; it += slots) {
       add(aq, Q + ((long long)h * N + t0 + tok) * d + lane * VEC);
       h += dh;
@@ -89,7 +95,7 @@ __global__ __launch_bounds__(kPoolThreads) void pool_sketch_kernel(
   }
   {
     int h = slot / cnt, tok = slot % cnt;
-#pragma unroll 8
+_Pragma(SW_STR(unroll SW_POOL_UNROLL))
     for (int it = slot; it < nk; it += slots) {
       add(ak, K + ((long long)h * N + t0 + tok) * d + lane * VEC);
       h += dh;
@@ -148,7 +154,11 @@ __global__ __launch_bounds__(kPoolThreads) void pool_sketch_kernel(
 
 // Four 16 x 16 tiles per workgroup, one per wavefront; the per-sequence max
 // |A| is reduced over the workgroup's tiles first, so a sequence receives one
-// atomicMax per workgroup.
+// atomicMax per workgroup. The k-range is taken in chunks of 64: in a chunk,
+// lane group q = l / 16 carries k = 64 c + 16 q + u in MFMA step u (the dot
+// product runs over every k once), so each lane reads 16 consecutive entries
+// of its row; every load of a chunk is issued before the first MFMA (indices
+// clamped, entries past r zeroed after the load).
 __global__ __launch_bounds__(256) void scores_kernel(const double* __restrict__ Qs,
                                                      const double* __restrict__ Ks, int r,
                                                      SeqMeta m,
@@ -179,13 +189,25 @@ __global__ __launch_bounds__(256) void scores_kernel(const double* __restrict__ 
       }
     } else {
       f64x4 acc = {0.0, 0.0, 0.0, 0.0};
-      const int ra = ti * 16 + (l & 15);
-      const int rb = tj * 16 + (l & 15);
-      for (int k0 = 0; k0 < r; k0 += 4) {
-        const int k = k0 + (l >> 4);
-        const double av = (ra < b && k < r) ? Qs[(long long)(bo + ra) * r + k] : 0.0;
-        const double bv = (rb < b && k < r) ? Ks[(long long)(bo + rb) * r + k] : 0.0;
-        acc = __builtin_amdgcn_mfma_f64_16x16x4f64(av, bv, acc, 0, 0, 0);
+      // rows past the sequence's last block are clamped (their results are
+      // not stored)
+      const double* qa = Qs + (long long)(bo + min(ti * 16 + (l & 15), b - 1)) * r;
+      const double* kb = Ks + (long long)(bo + min(tj * 16 + (l & 15), b - 1)) * r;
+      const int kq = 16 * (l >> 4);
+      for (int c0 = 0; c0 < r; c0 += 64) {
+        double av[16], bv[16];
+#pragma unroll
+        for (int u = 0; u < 16; ++u) {
+          const int k = min(c0 + kq + u, r - 1);
+          av[u] = qa[k];
+          bv[u] = kb[k];
+        }
+#pragma unroll
+        for (int u = 0; u < 16; ++u) {
+          const bool in = c0 + kq + u < r;
+          acc = __builtin_amdgcn_mfma_f64_16x16x4f64(in ? av[u] : 0.0, in ? bv[u] : 0.0, acc, 0,
+                                                     0, 0);
+        }
       }
       for (int v = 0; v < 4; ++v) {
         const int ri = ti * 16 + (l >> 4) + 4 * v, cj = tj * 16 + (l & 15);

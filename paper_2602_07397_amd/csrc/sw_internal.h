@@ -18,20 +18,26 @@ namespace sw {
 //   double qt[batch][r]          sketch of the current token's query
 //   double Qs[batch][b_max][r]   sketch of every query-block representative
 //   double Ks[batch][b_max][r]   sketch of every key-block representative
-//   float  A[batch][b_max][lda]  block-score cache, lda = b_max rounded up to 4
+//   float  rowc[batch][b_max]    the open block's score row A[b_cur][:] and
+//   float  colc[batch][b_max]    column A[:][b_cur] as the last step wrote
+//                                them (contiguous copies of cache entries)
+//   float  A[batch][lda/32][b_max][32]  block-score cache in strips of 32
+//                                columns (entry (m, j) at cache_at(b_max, m, j)
+//                                within a sequence), lda = b_max rounded up
+//                                to a multiple of 32
 // The step at position p reads the open-block means and counts of copy
 // (p + 1) % 2 (written by the step at p - 1) and writes copy p % 2, so every
 // workgroup of a step reads the previous values while one of them writes
 // the new ones.
 struct DecodeLayout {
-  int64_t scale, col0, cnt, bar, qt, qs, ks, a, total;
+  int64_t scale, col0, cnt, bar, qt, qs, ks, rowc, colc, a, total;
   int lda;
 };
 
 __host__ __device__ inline DecodeLayout decode_layout(int batch, int d, int r, int b_max) {
   auto al = [](int64_t x) { return (x + 255) / 256 * 256; };
   DecodeLayout L;
-  L.lda = (b_max + 3) & ~3;
+  L.lda = (b_max + 31) & ~31;
   int64_t o = 0;
   L.scale = o;  o = al(o + 8LL * batch);
   L.col0 = o;   o = al(o + 4LL * batch);
@@ -40,9 +46,18 @@ __host__ __device__ inline DecodeLayout decode_layout(int batch, int d, int r, i
   L.qt = o;     o = al(o + 8LL * batch * r);
   L.qs = o;     o = al(o + 8LL * batch * b_max * r);
   L.ks = o;     o = al(o + 8LL * batch * b_max * r);
+  L.rowc = o;   o = al(o + 4LL * batch * b_max);
+  L.colc = o;   o = al(o + 4LL * batch * b_max);
   L.a = o;      o = al(o + 4LL * batch * b_max * L.lda);
   L.total = o;
   return L;
+}
+
+// Offset (in floats) of score (m, j) within one sequence's cache: the cache
+// is stored as strips of 32 columns, each strip's rows contiguous (128 bytes
+// per row), so a walk over one strip's rows reads one contiguous range.
+__host__ __device__ inline int cache_at(int b_max, int m, int j) {
+  return ((j >> 5) * b_max + m) * 32 + (j & 31);
 }
 
 constexpr int kDecodeMaxSplits = 32;
@@ -89,13 +104,16 @@ hipError_t launch_decode_walk(const char* state, int batch, int d, int r, int b_
                               const int32_t* pos, int s_exp, bool relu, const double* r_prev,
                               double* r_out, hipStream_t st);
 
-// Alg. 2 steps 5-6 for the one-call decode step: the same walk row written to
-// rows [batch][b_max], normalised by the selection kernel, which then selects.
-hipError_t launch_decode_walk_select(const char* state, int batch, int d, int r, int b_max, int B,
-                                     const int32_t* pos, int s_exp, bool relu,
-                                     const double* r_prev, double* rows, int k, int pct,
-                                     uint32_t flags, int32_t* idx, int32_t* cnt, int kmax,
-                                     hipStream_t st);
+// Alg. 2 steps 1-6 of one layer for the one-call step: the incremental
+// sketch with the KV append, side by side with the walk over the score
+// entries the sketch leaves unchanged, then the walk row finished, normalised
+// and written to rows [batch][b_max], and its selection.
+hipError_t launch_decode_layer(int dtype, const void* q_new, const void* k_new, const void* v_new,
+                               void* Kc, void* Vc, int T_max, int batch, int h_q, int h_kv, int d,
+                               int B, const int32_t* pos, const int8_t* signs, const int32_t* cols,
+                               int r, int b_max, char* state, int s_exp, bool relu,
+                               const double* r_prev, double* rows, int k, int pct, uint32_t flags,
+                               int32_t* idx, int32_t* cnt, int kmax, hipStream_t st);
 
 hipError_t launch_select_decode(const double* rows, int batch, int b_max, int B,
                                 const int32_t* pos, int k, int pct, uint32_t flags, int32_t* idx,
