@@ -51,9 +51,12 @@ __device__ __forceinline__ void select_row_vals(const double (&v)[MAXE], int ava
                                                 int32_t* __restrict__ out,
                                                 int32_t* __restrict__ cnt, int kmax) {
   static_assert(MAXE <= 32, "one mask bit per value");
-  __shared__ int hist[256];
+  // the passes alternate between two copies of the histogram, the scan's
+  // wavefront totals and the boundary bin, so a pass needs three barriers
+  __shared__ int hist[2][256];
   __shared__ int scan_tmp[256];
-  __shared__ int sh_digit, sh_need, sh_cnt;
+  __shared__ int ptot[2][4];
+  __shared__ int sh_digit[2], sh_need[2], sh_cnt[2];
   __shared__ unsigned long long klo[4], khi[4];
   const int t = threadIdx.x;
   const int E = (avail + 255) / 256;
@@ -102,6 +105,7 @@ __device__ __forceinline__ void select_row_vals(const double (&v)[MAXE], int ava
       klo[t >> 6] = lo;
       khi[t >> 6] = hi;
     }
+    hist[0][t] = 0;
     __syncthreads();
 #pragma unroll
     for (int w = 0; w < 4; ++w) {
@@ -115,28 +119,32 @@ __device__ __forceinline__ void select_row_vals(const double (&v)[MAXE], int ava
     }
     for (int pass = same; pass < 8; ++pass) {
       const int shift = 56 - 8 * pass;
-      hist[t] = 0;
-      __syncthreads();
+      const int cur = (pass - same) & 1;
 #pragma unroll
       for (int e = 0; e < MAXE; ++e)
         if ((candmask >> e) & 1u)
-          if ((key[e] & pmask) == prefix) atomicAdd(&hist[(int)((key[e] >> shift) & 255ull)], 1);
+          if ((key[e] & pmask) == prefix)
+            atomicAdd(&hist[cur][(int)((key[e] >> shift) & 255ull)], 1);
+      hist[cur ^ 1][t] = 0;                // the next pass's copy
       __syncthreads();
-      const int v = hist[255 - t];
-      int total;
-      const int excl = block_exclusive_scan_256(v, scan_tmp, &total);
+      // bins in descending digit order, exclusive prefix counts
+      const int v = hist[cur][255 - t];
+      const int x = wave_inclusive_scan(v);
+      if ((t & 63) == 63) ptot[cur][t >> 6] = x;
+      __syncthreads();
+      int excl = x - v;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) excl += (q < (t >> 6)) ? ptot[cur][q] : 0;
       if (v > 0 && excl < need && need <= excl + v) {
-        sh_digit = 255 - t;
-        sh_need = need - excl;
-        sh_cnt = v;
+        sh_digit[cur] = 255 - t;
+        sh_need[cur] = need - excl;
+        sh_cnt[cur] = v;
       }
       __syncthreads();
-      prefix |= ((unsigned long long)sh_digit) << shift;
+      prefix |= ((unsigned long long)sh_digit[cur]) << shift;
       pmask |= 255ull << shift;
-      need = sh_need;
-      const bool done = (sh_need == sh_cnt);
-      __syncthreads();
-      if (done) {
+      need = sh_need[cur];
+      if (sh_need[cur] == sh_cnt[cur]) {
         take_all_eq = true;
         break;
       }
