@@ -481,6 +481,19 @@ __device__ __forceinline__ void walk_old_body(const char* __restrict__ state, in
   const int bytes = b_max * lda * 4;
   const __amdgpu_buffer_rsrc_t ra =
       __builtin_amdgcn_make_buffer_rsrc((void*)A, (short)0, bytes, kStripBufWord3);
+  // The decode-filled columns before b_cur of strip sb over the rows above
+  // it (rows < 32 sb): the loads of the first such quad over the first 2048
+  // rows go out before the strip's own rows, so their latency is hidden.
+  const int xjb = sb * kStripCols;
+  const int jlo_b = max(col0, xjb), jhi_b = min(bc - 1, xjb + kStripCols - 1);
+  const bool pre_b = sb != sa && xjb > 0 && jlo_b <= jhi_b;
+  const int jd_b = xjb + 4 * ((jlo_b - xjb) / 4);
+  uint4 pa[8];
+#pragma unroll
+  for (int v = 0; v < 8; ++v) {
+    const int m = t + v * kStripThreads;
+    pa[v] = load_quad(ra, (pre_b && m < xjb) ? cache_at(b_max, m, jd_b) * 4 : bytes);
+  }
   double acc[4] = {0.0, 0.0, 0.0, 0.0};
   __syncthreads();                       // the staged row is visible
   const double* rp = smem;
@@ -523,10 +536,15 @@ __device__ __forceinline__ void walk_old_body(const char* __restrict__ state, in
       double xa[4] = {0.0, 0.0, 0.0, 0.0};
       for (int m1 = t; m1 < xj0; m1 += 8 * kStripThreads) {
         uint4 a[8];
+        if (which == 1 && jd == jd_b && m1 == t) {   // loaded before the strip's rows
 #pragma unroll
-        for (int v = 0; v < 8; ++v) {
-          const int m = m1 + v * kStripThreads;
-          a[v] = load_quad(ra, m < xj0 ? cache_at(b_max, m, jd) * 4 : bytes);
+          for (int v = 0; v < 8; ++v) a[v] = pa[v];
+        } else {
+#pragma unroll
+          for (int v = 0; v < 8; ++v) {
+            const int m = m1 + v * kStripThreads;
+            a[v] = load_quad(ra, m < xj0 ? cache_at(b_max, m, jd) * 4 : bytes);
+          }
         }
 #pragma unroll
         for (int v = 0; v < 8; ++v) {
