@@ -136,13 +136,24 @@ __global__ __launch_bounds__(256) void walk_gemm_kernel(const double* __restrict
   // w, w + 4, w + 8, ...; its chunks are double-buffered in registers: the
   // loads of the next chunk are in flight during the MFMAs of the current one.
   const int kq = l >> 4;
-  const long long rowA = (long long)ra * b;
+  const long long rowA = (long long)min(ra, b - 1) * b;
+  const int cbc = min(cb, b - 1);
+  // the loads carry no condition (indices clamped into the matrix; the
+  // entries outside the causal range are zeroed after loading), so all of a
+  // chunk's loads are in flight together
   auto load = [&](int k0, double (&av)[8], double (&bv)[8]) {
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
       const int k = k0 + 8 * kq + u;
-      av[u] = (ra < b && k <= ra) ? Ps[rowA + k] : 0.0;
-      bv[u] = (k < b && cb <= k) ? As[(long long)k * b + cb] : 0.0;
+      const int kc = min(k, b - 1);
+      av[u] = Ps[rowA + kc];
+      bv[u] = As[(long long)kc * b + cbc];
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int k = k0 + 8 * kq + u;
+      av[u] = (ra < b && k <= ra) ? av[u] : 0.0;
+      bv[u] = (k < b && cb <= k) ? bv[u] : 0.0;
     }
   };
   f64x4 acc = {0.0, 0.0, 0.0, 0.0};

@@ -33,6 +33,34 @@ def test_decode_step_is_bit_identical_to_per_layer_calls(dtype, h_q, h_kv, d, va
     w = synth.Workload("dec", 45, layers=3, h_q=h_q, h_kv=h_kv, d=d, B=64, dtype=dtype, pct=20,
                        needles=2, batch=3, kv_len=1000, steps=70)
     run = D.DecodeRun(w, prompts=[1000, 640, 65], steps=70, variant=variant)
+    _check_against_per_layer(w, run, dtype, h_q, h_kv, d, variant)
+
+
+def test_decode_step_with_decode_columns_across_strips():
+    """Blocks of 16 tokens, so that decode fills several columns of the score
+    cache: 193..199 inside one 32-column strip (two column quads, the rows
+    above the strip), and 62..68 across the boundary of strips 1 and 2; the
+    cache has 7 strips (three pairs and a single strip)."""
+    w = synth.Workload("dec", 48, layers=2, h_q=4, h_kv=1, d=64, B=16, dtype="bf16", pct=20,
+                       needles=2, batch=2, kv_len=3100, steps=100)
+    run = D.DecodeRun(w, prompts=[3100, 1000], steps=100)
+    _check_against_per_layer(w, run, "bf16", 4, 1, 64, sw.WALK_POWER)
+
+
+def test_decode_step_with_a_long_cache():
+    """2307 blocks of 16 tokens (the selection holds 16 values per thread):
+    the open block moves from 2303 to 2304 during the run, so the closed
+    decode column 2303 lies in strip 71 and the open one in strip 72, and
+    the rows above strip 71 (2272) extend past the 2048 whose loads the walk
+    issues ahead."""
+    w = synth.Workload("dec", 47, layers=2, h_q=4, h_kv=1, d=64, B=16, dtype="bf16", pct=20,
+                       needles=2, batch=1, kv_len=36858, steps=12)
+    run = D.DecodeRun(w, prompts=[36858], steps=12, T_extra=42)
+    assert run.b_max == 2307
+    _check_against_per_layer(w, run, "bf16", 4, 1, 64, sw.WALK_POWER)
+
+
+def _check_against_per_layer(w, run, dtype, h_q, h_kv, d, variant):
     Kc = torch.stack(run.Kc).contiguous()
     Vc = torch.stack(run.Vc).contiguous()
     state = torch.stack(run.state).contiguous()
