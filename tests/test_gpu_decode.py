@@ -19,9 +19,10 @@ U = pytest.importorskip("_gpu_util")
 class DecodeRun:
     """Runs the same decode on the GPU (through the C ABI) and on the oracle."""
 
-    def __init__(self, w, prompts, steps, T_extra=0, variant=sw.WALK_POWER):
+    def __init__(self, w, prompts, steps, T_extra=0, variant=sw.WALK_POWER, s=None):
         self.w = w
         self.variant = variant
+        self.s = w.s if s is None else s
         self.B = w.B
         self.d = w.d
         self.r = w.r
@@ -72,10 +73,11 @@ class DecodeRun:
             sw.sketch_scores_decode(qd, kd, self.B, pos, self.ts, self.tc, self.b_max, self.state[l])
             if self.variant == sw.WALK_POWER:
                 r_gpu = sw.walk_update_decode(self.state[l], self.batch, w.d, w.r, self.b_max, self.B,
-                                              pos, w.s, r_prev=r_gpu)
+                                              pos, self.s, r_prev=r_gpu)
             else:
                 r_gpu = sw.walk_update_decode_variant(self.variant, self.state[l], self.batch, w.d,
-                                                      w.r, self.b_max, self.B, pos, w.s, r_prev=r_gpu)
+                                                      w.r, self.b_max, self.B, pos, self.s,
+                                                      r_prev=r_gpu)
             idx, cnt, _ = sw.select_topk_blocks_decode(r_gpu, self.B, pos, density_pct=w.pct,
                                                        kmax=self.kmax)
             out = sw.sparse_attn_decode(qd, self.Kc[l], self.Vc[l], self.B, pos, idx, cnt, self.kmax)
@@ -92,7 +94,7 @@ class DecodeRun:
                 self.Kh[l][b][:, p] = kh[b]
                 self.Vh[l][b][:, p] = vh[b]
                 row, sel, gap = O.decode_layer_step(self.ost[l][b], qh[b], kh[b], p, r_ref[b], self.B,
-                                                    self.signs, self.cols, w.s, pct=w.pct,
+                                                    self.signs, self.cols, self.s, pct=w.pct,
                                                     variant=self.variant)
                 r_ref[b] = row
                 stats["werr"] = max(stats["werr"], U.max_abs(rg[b, :bc + 1], row))

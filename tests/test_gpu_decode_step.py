@@ -70,9 +70,9 @@ def _check_against_per_layer(w, run, dtype, h_q, h_kv, d, variant):
     for k in range(run.steps):
         q, kk, v = _stacked_inputs(w, k, run.batch)
         pos = U.to_dev(np.array([n + k for n in run.prompts], dtype=np.int32))
-        out = sw.decode_step(q, kk, v, Kc, Vc, state, pos, run.ts, run.tc, run.B, run.b_max, s=w.s,
-                             walk_variant=variant, density_pct=w.pct, kmax=run.kmax, out=out,
-                             workspace=ws)
+        out = sw.decode_step(q, kk, v, Kc, Vc, state, pos, run.ts, run.tc, run.B, run.b_max,
+                             s=run.s, walk_variant=variant, density_pct=w.pct, kmax=run.kmax,
+                             out=out, workspace=ws)
         st = run.step(k)                           # per-layer path, checked against the oracle
         for l, (r, idx, cnt, o) in enumerate(run.last):
             assert torch.equal(out["rows"][l], r), (k, l)
