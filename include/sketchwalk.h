@@ -354,10 +354,11 @@ int sw_sparse_attn_decode_noalloc(int dtype, const void* q, const void* Kc, cons
  * from that of layer l-1; layer 0 is the first walked layer). Per layer it
  * enqueues the same arithmetic as sw_kv_append + sw_sketch_scores_decode +
  * sw_walk_update_decode_variant + sw_select_topk_blocks_decode +
- * sw_sparse_attn_decode, with the KV append and the score updates in one
- * kernel and the walk row's normalisation fused into the selection (5 kernel
- * launches per layer instead of 7); results are bit-identical to those
- * calls.
+ * sw_sparse_attn_decode, with the KV append, the score updates and the walk
+ * over the score entries the step leaves unchanged in one launch, and the
+ * open block's walk terms and the normalisation in the selection's launch
+ * (4 kernel launches per layer instead of 7); results are bit-identical to
+ * those calls.
  *
  * Layer-stacked, contiguous buffers (device):
  *   q_new [layers][batch][h_q][d], k_new, v_new [layers][batch][h_kv][d]
