@@ -19,7 +19,8 @@
 //                         cache; one workgroup per (sequence, pair of
 //                         32-column strips), the pairs balanced so that every
 //                         workgroup reads about as many rows, 32 row groups
-//                         reduced in LDS in a fixed order; the rows above a
+//                         reduced in a fixed order (lane exchanges within a
+//                         wavefront, then the wavefronts); the rows above a
 //                         strip, which hold only its decode-filled columns,
 //                         are shared by every thread of the workgroup
 //  decode_sketch_walk_kernel  the one-call step's launch of both: the walk
@@ -359,10 +360,7 @@ __global__ __launch_bounds__(256) void decode_sketch_kernel(const T* __restrict_
 
 constexpr int kStripCols = 32;           // columns per strip: one 128-byte piece of a row
 constexpr int kStripQuads = kStripCols / 4;
-#ifndef SW_STRIP_GROUPS
-#define SW_STRIP_GROUPS 32               // row groups per workgroup
-#endif
-constexpr int kStripGroups = SW_STRIP_GROUPS;
+constexpr int kStripGroups = 32;         // row groups per workgroup, 8 per wavefront
 constexpr int kStripThreads = kStripQuads * kStripGroups;
 #ifndef SW_STRIP_ROWS
 #define SW_STRIP_ROWS 4                  // rows each thread loads before adding
@@ -406,20 +404,18 @@ __device__ __forceinline__ uint4 load_quad(__amdgpu_buffer_rsrc_t ra, int off) {
 // (m < 32 x): those rows hold nothing else in the strip, so every thread of
 // the workgroup takes a share of them, for those columns only.
 // r_out[j] = (sum over the strip's rows: per group ascending, then over the
-// strip's groups in blocks of 8, then over the blocks) + (sum over the rows
-// above: per thread ascending, then over the threads in blocks of 16, then
-// over the blocks) of r_prev[m] W[m][j] for j < b_cur. Entries the cache
+// 8 groups of a wavefront by a butterfly of lane exchanges, then over the
+// four wavefronts in order) + (sum over the rows above: per thread
+// ascending, then a butterfly over the 64 lanes, then the four wavefronts in
+// order) of r_prev[m] W[m][j] for j < b_cur. Entries the cache
 // holds as zero (above the diagonal outside the decode-filled columns) give
 // zero terms; quads that are wholly zero are not loaded.
-constexpr int kWalkSmem = kStripGroups * kStripCols > SW_MAX_BLOCKS ? kStripGroups * kStripCols
-                                                                    : SW_MAX_BLOCKS;
-constexpr int kWalkBlk = kStripGroups / 8;
-// LDS of one walk workgroup (doubles): the staged previous row, reused for the
-// row groups' sums; the block sums; the rows-above sums per thread, per block
-// of 16 threads and per column
-constexpr int kWalkLdsDoubles =
-    kWalkSmem + 2 * kWalkBlk * kStripCols + kStripThreads * 4 + (kStripThreads / 16) * 4 +
-    2 * kStripCols;
+// LDS of one walk workgroup (doubles): the staged previous walk row, then
+// per wavefront and strip the strip-row sums and the rows-above sums of the
+// 32 columns.
+constexpr int kWalkSmem = SW_MAX_BLOCKS;
+constexpr int kWalkLdsDoubles = kWalkSmem + 2 * (kStripThreads / 64) * 2 * kStripCols;
+static_assert(kStripThreads == 256 && kStripQuads == 8, "8 row groups x 8 quads per wavefront");
 
 template <bool S8, bool RELU>
 __device__ __forceinline__ void walk_old_body(const char* __restrict__ state, int batch, int d,
@@ -429,11 +425,10 @@ __device__ __forceinline__ void walk_old_body(const char* __restrict__ state, in
                                               double* __restrict__ r_out, int bi, int k,
                                               double* lds) {
   double* smem = lds;
-  double (*red2)[kWalkBlk][kStripCols] =
-      reinterpret_cast<double (*)[kWalkBlk][kStripCols]>(smem + kWalkSmem);
-  double (*xr)[4] = reinterpret_cast<double (*)[4]>(smem + kWalkSmem + 2 * kWalkBlk * kStripCols);
-  double (*xred)[4] = xr + kStripThreads;
-  double (*xsum)[kStripCols] = reinterpret_cast<double (*)[kStripCols]>(xred + kStripThreads / 16);
+  // wsum[w][strip][c]: wavefront w's strip-row sums; xw[w][strip][c]: its
+  // rows-above sums (zero outside the decode-filled quads)
+  double (*wsum)[2][kStripCols] = reinterpret_cast<double (*)[2][kStripCols]>(smem + kWalkSmem);
+  double (*xw)[2][kStripCols] = wsum + kStripThreads / 64;
   const DecodeLayout L = decode_layout(batch, d, r, b_max);
   const int lda = L.lda;
   const int t = threadIdx.x;
@@ -519,10 +514,12 @@ __device__ __forceinline__ void walk_old_body(const char* __restrict__ state, in
       }
     }
   }
+  // Both sums are reduced in a fixed order behind one barrier: per wavefront
+  // by lane exchanges (a butterfly), then over the four wavefronts in order.
+  const int wv = t >> 6, lane = t & 63;
+  xw[wv][lane >> 5][lane & 31] = 0.0;
   // the decode-filled columns before b_cur of each strip over the rows above
   // it (rows 0 .. 32 x - 1), one quad at a time, every thread a share of rows
-  if (t < 2 * kStripCols) xsum[t / kStripCols][t % kStripCols] = 0.0;
-  __syncthreads();
 #pragma unroll 1
   for (int which = 0; which < 2; ++which) {
     const int xs = which ? sb : sa;
@@ -556,59 +553,45 @@ __device__ __forceinline__ void walk_old_body(const char* __restrict__ state, in
             if (jd + e != bc) xa[e] += rv * walk_weight<S8, RELU>(av[e], inv_c, s_exp);
         }
       }
-      // fixed-order reduction over the threads: blocks of 16, then the blocks
+      for (int off = 1; off < 64; off <<= 1)
 #pragma unroll
-      for (int e = 0; e < 4; ++e) xr[t][e] = xa[e];
-      __syncthreads();
-      if (t < (kStripThreads / 16) * 4) {
-        const int bk = t / 4, e = t % 4;
-        double v = 0.0;
+        for (int e = 0; e < 4; ++e) xa[e] += __shfl_xor(xa[e], off);
+      if (lane == 0)
 #pragma unroll
-        for (int u = 0; u < 16; ++u) v += xr[bk * 16 + u][e];
-        xred[bk][e] = v;
-      }
-      __syncthreads();
-      if (t < 4) {
-        double v = 0.0;
-#pragma unroll
-        for (int u = 0; u < kStripThreads / 16; ++u) v += xred[u][t];
-        xsum[which][4 * qd + t] = v;
-      }
-      __syncthreads();
+        for (int e = 0; e < 4; ++e) xw[wv][which][4 * qd + e] = xa[e];
     }
   }
-  __syncthreads();
-  double* red = smem;                    // [kStripGroups][kStripCols]
-#pragma unroll
-  for (int e = 0; e < 4; ++e) red[g * kStripCols + 4 * q + e] = acc[e];
-  __syncthreads();
-  // fixed-order reduction over a strip's groups: sums of 8 consecutive groups
-  // (one per thread: strip, block of 8 groups, column), then of the blocks
+  // the strip rows: the 8 row groups of a wavefront (lanes q, q + 8, ...,
+  // q + 56 hold column quad q), per strip
   {
-    const int which = t / (kWalkBlk * kStripCols), bk = (t / kStripCols) % kWalkBlk,
-              c = t % kStripCols;
-    const int g0 = which ? ga : 0, g1 = which ? kStripGroups : ga;
-    double vals[8];
+    double s0[4], s1[4];
 #pragma unroll
-    for (int u = 0; u < 8; ++u) vals[u] = red[(bk * 8 + u) * kStripCols + c];
-    double v = 0.0;
+    for (int e = 0; e < 4; ++e) {
+      s0[e] = in_a ? acc[e] : 0.0;
+      s1[e] = in_a ? 0.0 : acc[e];
+    }
+    for (int off = kStripQuads; off < 64; off <<= 1)
 #pragma unroll
-    for (int u = 0; u < 8; ++u) v += (bk * 8 + u >= g0 && bk * 8 + u < g1) ? vals[u] : 0.0;
-    red2[which][bk][c] = v;
+      for (int e = 0; e < 4; ++e) {
+        s0[e] += __shfl_xor(s0[e], off);
+        s1[e] += __shfl_xor(s1[e], off);
+      }
+    if (lane < kStripQuads)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        wsum[wv][0][4 * lane + e] = s0[e];
+        wsum[wv][1][4 * lane + e] = s1[e];
+      }
   }
   __syncthreads();
   if (t < 2 * kStripCols) {
     const int which = t / kStripCols, c = t % kStripCols;
     if (which == 0 || sb != sa) {
       const int xs = which ? sb : sa;
-      double vals[kWalkBlk];
-#pragma unroll
-      for (int u = 0; u < kWalkBlk; ++u) vals[u] = red2[which][u][c];
-      double v = 0.0;
-#pragma unroll
-      for (int u = 0; u < kWalkBlk; ++u) v += vals[u];
+      double v = ((wsum[0][which][c] + wsum[1][which][c]) + wsum[2][which][c]) + wsum[3][which][c];
       const int jj = xs * kStripCols + c;
-      if (jj >= col0 && xs * kStripCols > 0) v += xsum[which][c];
+      if (jj >= col0 && xs * kStripCols > 0)
+        v += ((xw[0][which][c] + xw[1][which][c]) + xw[2][which][c]) + xw[3][which][c];
       if (jj < bc) r_out[(long long)bi * b_max + jj] = v;
     }
   }
